@@ -1,0 +1,241 @@
+// C ABI device entry points: validation, upload of the plan tables into the
+// caller's workspace, and the launch sequence of one forward / backward call.
+#include <string>
+
+#include "ba_internal.h"
+#include "kernels.h"
+
+namespace ba {
+namespace {
+
+int fail(int code, const std::string& msg) {
+  set_error(msg);
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(BA_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// every device tensor is read in 16-byte vectors
+int check_ptr(const void* p, bool needed, const char* name) {
+  if (!needed) return BA_OK;
+  if (!p) return fail(BA_E_INVAL, std::string(name) + " is NULL");
+  if (!aligned16(p)) return fail(BA_E_INVAL, std::string(name) + " is not 16-byte aligned");
+  return BA_OK;
+}
+
+struct Common {
+  int rc = BA_OK;
+  WorkspaceLayout w;
+  char* ws = nullptr;
+};
+
+Common prepare(const ba_plan* plan, int32_t mode, void* workspace, size_t ws_bytes, bool bwd,
+               hipStream_t stream) {
+  Common c;
+  if (!plan) {
+    c.rc = fail(BA_E_INVAL, "plan is NULL");
+    return c;
+  }
+  if (mode != BA_MODE_PER_STEP && mode != BA_MODE_FUSED) {
+    c.rc = fail(BA_E_INVAL, "unknown mode");
+    return c;
+  }
+  const Plan& P = plan->p;
+  if (P.cp_size > kMaxCp) {
+    c.rc = fail(BA_E_UNSUPPORTED, "cp_size > 32 unsupported");
+    return c;
+  }
+  c.w = workspace_layout(P, mode);
+  const size_t need = bwd ? c.w.bwd_total : c.w.fwd_total;
+  if (!workspace || ws_bytes < need) {
+    c.rc = fail(BA_E_WORKSPACE, "workspace of " + std::to_string(ws_bytes) + " bytes, need " +
+                                    std::to_string(need));
+    return c;
+  }
+  if (((uintptr_t)workspace & 255) != 0) {
+    c.rc = fail(BA_E_WORKSPACE, "workspace must be 256-byte aligned");
+    return c;
+  }
+  c.ws = static_cast<char*>(workspace);
+  if (!P.image.empty()) {
+    hipError_t e = hipMemcpyAsync(c.ws + c.w.tables, P.image.data(), P.image.size(), hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) c.rc = hip_fail(e, "upload of plan tables");
+  }
+  return c;
+}
+
+}  // namespace
+}  // namespace ba
+
+using namespace ba;
+
+extern "C" int branch_attn_fwd(void* stream_, const ba_plan* plan, int32_t mode, const ba_fwd_io* io,
+                               void* workspace, size_t workspace_bytes) {
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+  if (!io) return fail(BA_E_INVAL, "io is NULL");
+  if (!plan) return fail(BA_E_INVAL, "plan is NULL");
+  const Plan& P = plan->p;
+  const bool has_main = P.any_main_query;   // some sequence's main tokens are queries
+  const bool has_keys = P.n_local > 0;      // main keys exist
+  const bool has_br = P.num_branch_rows > 0 && !P.groups.empty();
+  int rc;
+  if ((rc = check_ptr(io->q_main, has_main, "q_main")) || (rc = check_ptr(io->o_main, has_main, "o_main")) ||
+      (rc = check_ptr(io->lse_main, has_main, "lse_main")) || (rc = check_ptr(io->q_br, has_br, "q_br")) ||
+      (rc = check_ptr(io->k_br, has_br, "k_br")) || (rc = check_ptr(io->v_br, has_br, "v_br")) ||
+      (rc = check_ptr(io->o_br, has_br, "o_br")) || (rc = check_ptr(io->lse_br, has_br, "lse_br")))
+    return rc;
+  if (has_keys && (!io->k_step || !io->v_step)) return fail(BA_E_INVAL, "k_step / v_step missing");
+  if (P.toks.empty()) return BA_OK;
+  Common c = prepare(plan, mode, workspace, workspace_bytes, false, stream);
+  if (c.rc) return c.rc;
+
+  FwdParams p{};
+  p.seqs = reinterpret_cast<const SeqInfo*>(c.ws + c.w.tables + P.off_seqs);
+  p.toks = reinterpret_cast<const TokInfo*>(c.ws + c.w.tables + P.off_toks);
+  p.groups = reinterpret_cast<const GroupInfo*>(c.ws + c.w.tables + P.off_groups);
+  p.tiles = reinterpret_cast<const FwdTile*>(c.ws + c.w.tables + P.off_fwd);
+  p.num_tiles = (int32_t)P.fwd_tiles.size();
+  p.C = P.cp_size;
+  p.rank = P.cp_rank;
+  p.hq = P.hq;
+  p.hkv = P.hkv;
+  p.G = P.group;
+  p.scale_log2 = P.scale * kLog2e;
+  p.n_local = P.n_local;
+  p.n_br = P.num_branch_rows;
+  p.q_main = static_cast<const bf16*>(io->q_main);
+  p.q_br = static_cast<const bf16*>(io->q_br);
+  p.k_br = static_cast<const bf16*>(io->k_br);
+  p.v_br = static_cast<const bf16*>(io->v_br);
+  for (int j = 0; j < P.cp_size && has_keys; ++j) {
+    if ((rc = check_ptr(io->k_step[j], has_keys, "k_step[j]")) || (rc = check_ptr(io->v_step[j], has_keys, "v_step[j]")))
+      return rc;
+    p.k_step[j] = static_cast<const bf16*>(io->k_step[j]);
+    p.v_step[j] = static_cast<const bf16*>(io->v_step[j]);
+  }
+  p.o_main = static_cast<bf16*>(io->o_main);
+  p.o_br = static_cast<bf16*>(io->o_br);
+  p.lse_main = io->lse_main;
+  p.lse_br = io->lse_br;
+  hipError_t e;
+  if (mode == BA_MODE_FUSED) {
+    p.step_first = 0;
+    p.step_count = P.cp_size;
+    if ((e = launch_fwd(p, kModeFused, stream)) != hipSuccess) return hip_fail(e, "forward launch");
+    return BA_OK;
+  }
+  p.o_acc = reinterpret_cast<float*>(c.ws + c.w.o_acc);
+  p.lse_acc = reinterpret_cast<float*>(c.ws + c.w.lse_acc);
+  for (int i = 0; i < P.cp_size; ++i) {
+    p.step_first = i;
+    p.step_count = 1;
+    p.acc_first = i == 0;
+    if ((e = launch_fwd(p, kModeStep, stream)) != hipSuccess) return hip_fail(e, "ring-step launch");
+  }
+  p.step_first = 0;
+  p.step_count = 0;
+  if ((e = launch_fwd(p, kModeFinal, stream)) != hipSuccess) return hip_fail(e, "branch/merge launch");
+  return BA_OK;
+}
+
+extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode, const ba_bwd_io* io,
+                               void* workspace, size_t workspace_bytes) {
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+  if (!io) return fail(BA_E_INVAL, "io is NULL");
+  if (!plan) return fail(BA_E_INVAL, "plan is NULL");
+  const Plan& P = plan->p;
+  const bool has_main = P.any_main_query;
+  const bool has_keys = P.n_local > 0;
+  const bool has_br = P.num_branch_rows > 0 && !P.groups.empty();
+  if (io->grad_dtype != BA_DTYPE_BF16 && io->grad_dtype != BA_DTYPE_F32)
+    return fail(BA_E_INVAL, "grad_dtype must be BA_DTYPE_BF16 or BA_DTYPE_F32");
+  int rc;
+  if ((rc = check_ptr(io->q_main, has_main, "q_main")) || (rc = check_ptr(io->o_main, has_main, "o_main")) ||
+      (rc = check_ptr(io->lse_main, has_main, "lse_main")) || (rc = check_ptr(io->do_main, has_main, "do_main")) ||
+      (rc = check_ptr(io->dq_main, has_main, "dq_main")) || (rc = check_ptr(io->q_br, has_br, "q_br")) ||
+      (rc = check_ptr(io->k_br, has_br, "k_br")) || (rc = check_ptr(io->v_br, has_br, "v_br")) ||
+      (rc = check_ptr(io->o_br, has_br, "o_br")) || (rc = check_ptr(io->lse_br, has_br, "lse_br")) ||
+      (rc = check_ptr(io->do_br, has_br, "do_br")) || (rc = check_ptr(io->dq_br, has_br, "dq_br")) ||
+      (rc = check_ptr(io->dk_br, has_br, "dk_br")) || (rc = check_ptr(io->dv_br, has_br, "dv_br")))
+    return rc;
+  if (has_keys && (!io->k_step || !io->v_step || !io->dk_step || !io->dv_step))
+    return fail(BA_E_INVAL, "k_step / v_step / dk_step / dv_step missing");
+  Common c{};
+  if (P.cp_size > kMaxCp) return fail(BA_E_UNSUPPORTED, "cp_size > 32 unsupported");
+  BwdParams p{};
+  hipError_t e;
+  // the per-step KV gradients are overwritten: clear the rows no work item writes
+  const size_t elem = io->grad_dtype == BA_DTYPE_F32 ? 4 : 2;
+  const size_t step_bytes = (size_t)P.n_local * P.hkv * kHeadDim * elem;
+  for (int j = 0; j < P.cp_size && has_keys; ++j) {
+    if ((rc = check_ptr(io->k_step[j], true, "k_step[j]")) || (rc = check_ptr(io->v_step[j], true, "v_step[j]")) ||
+        (rc = check_ptr(io->dk_step[j], true, "dk_step[j]")) || (rc = check_ptr(io->dv_step[j], true, "dv_step[j]")))
+      return rc;
+    p.k_step[j] = static_cast<const bf16*>(io->k_step[j]);
+    p.v_step[j] = static_cast<const bf16*>(io->v_step[j]);
+    p.dk_step[j] = io->dk_step[j];
+    p.dv_step[j] = io->dv_step[j];
+  }
+  if (P.toks.empty() && !has_keys) return BA_OK;
+  c = prepare(plan, mode, workspace, workspace_bytes, true, stream);
+  if (c.rc) return c.rc;
+  for (int j = 0; j < P.cp_size && has_keys; ++j) {
+    if ((e = launch_zero(io->dk_step[j], step_bytes, stream)) != hipSuccess) return hip_fail(e, "clear dk");
+    if ((e = launch_zero(io->dv_step[j], step_bytes, stream)) != hipSuccess) return hip_fail(e, "clear dv");
+  }
+  if (P.toks.empty()) return BA_OK;
+  p.seqs = reinterpret_cast<const SeqInfo*>(c.ws + c.w.tables + P.off_seqs);
+  p.toks = reinterpret_cast<const TokInfo*>(c.ws + c.w.tables + P.off_toks);
+  p.groups = reinterpret_cast<const GroupInfo*>(c.ws + c.w.tables + P.off_groups);
+  const BwdTile* tiles = reinterpret_cast<const BwdTile*>(c.ws + c.w.tables + P.off_bwd);
+  p.C = P.cp_size;
+  p.rank = P.cp_rank;
+  p.hq = P.hq;
+  p.hkv = P.hkv;
+  p.G = P.group;
+  p.num_tokens = (int32_t)P.toks.size();
+  p.num_groups = (int32_t)P.groups.size();
+  p.scale = P.scale;
+  p.scale_log2 = P.scale * kLog2e;
+  p.n_local = P.n_local;
+  p.n_br = P.num_branch_rows;
+  p.q_main = static_cast<const bf16*>(io->q_main);
+  p.q_br = static_cast<const bf16*>(io->q_br);
+  p.k_br = static_cast<const bf16*>(io->k_br);
+  p.v_br = static_cast<const bf16*>(io->v_br);
+  p.o_main = static_cast<const bf16*>(io->o_main);
+  p.o_br = static_cast<const bf16*>(io->o_br);
+  p.lse_main = io->lse_main;
+  p.lse_br = io->lse_br;
+  p.do_main = static_cast<const bf16*>(io->do_main);
+  p.do_br = static_cast<const bf16*>(io->do_br);
+  p.dq_main = io->dq_main;
+  p.dq_br = io->dq_br;
+  p.dk_br = io->dk_br;
+  p.dv_br = io->dv_br;
+  p.grad_f32 = io->grad_dtype == BA_DTYPE_F32;
+  p.rowstat = reinterpret_cast<float2*>(c.ws + c.w.rowstat);
+  p.dq_acc = reinterpret_cast<float*>(c.ws + c.w.dq_acc);
+
+  if ((e = launch_bwd_preprocess(p, stream)) != hipSuccess) return hip_fail(e, "preprocess launch");
+  if (mode == BA_MODE_FUSED) {
+    p.tiles = tiles;
+    p.num_tiles = (int32_t)P.bwd_tiles.size();
+    if ((e = launch_bwd_main(p, stream)) != hipSuccess) return hip_fail(e, "backward launch");
+  } else {
+    for (int i = 0; i < P.cp_size; ++i) {
+      p.tiles = tiles + P.bwd_step_off[i];
+      p.num_tiles = P.bwd_step_off[i + 1] - P.bwd_step_off[i];
+      if ((e = launch_bwd_main(p, stream)) != hipSuccess) return hip_fail(e, "ring-step backward launch");
+    }
+  }
+  if (has_br) {
+    if ((e = launch_bwd_branch(p, P.max_group_len, stream)) != hipSuccess) return hip_fail(e, "branch backward launch");
+  }
+  if ((e = launch_bwd_finalize(p, stream)) != hipSuccess) return hip_fail(e, "finalize launch");
+  return BA_OK;
+}

@@ -1,0 +1,131 @@
+// Internal data structures shared by the host planner and the gfx950 kernels.
+//
+// The planner turns a rank share (Sec. 3.2 of the paper: main queries of the
+// rank's two zigzag chunks, branch groups anchored there) into flat tables
+// that the kernels index directly:
+//   * SeqInfo   -- per sequence: where its keys sit in every ring-step block
+//                  and which slice of the token table holds its queries;
+//   * TokInfo   -- per query token, ordered by causal limit P within a
+//                  sequence (main token at p has P = p; a branch member has
+//                  P = anchor), so that every key tile is read by a
+//                  contiguous range of tokens;
+//   * GroupInfo -- per branch group: member rows and kind;
+//   * FwdTile   -- a forward work item: up to kFwdRows / G tokens times the G
+//                  query heads of one KV head;
+//   * BwdTile   -- a backward work item: kBwdKeys keys of one ring-step
+//                  block, one sequence and one KV head, plus the range of
+//                  query tokens that reach them.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/branch_attn.h"
+
+namespace ba {
+
+// tile shapes (the kernels are written for exactly these)
+constexpr int kHeadDim = 128;
+constexpr int kFwdRows = 128;   // query rows (token x head) per forward tile
+constexpr int kFwdKeys = 64;    // keys per forward inner iteration
+constexpr int kBwdKeys = 128;   // keys owned by one backward work item
+constexpr int kBwdRows = 64;    // query rows per backward inner iteration
+
+struct SeqInfo {
+  int32_t seg_off;    // offset of the sequence in every rank-local main array
+  int32_t c;          // zigzag chunk length L / (2 C)
+  int32_t tok_begin;  // query tokens of the sequence: [tok_begin, tok_end)
+  int32_t tok_end;
+};
+
+struct TokInfo {
+  int32_t qrow;  // >= 0: rank-local main row; < 0: branch row (-qrow - 1)
+  int32_t P;     // causal limit: keys at positions 0..P are visible
+  int32_t grp;   // branch group, -1 for a main token
+  int32_t gidx;  // member index inside the group
+};
+
+struct GroupInfo {
+  int32_t row0;
+  int32_t stride;
+  int32_t len;
+  int32_t kind;
+  int32_t tok0;  // token-table index of member 0 (members are consecutive)
+  int32_t pad[3];
+};
+
+struct FwdTile {
+  int32_t seq;
+  int32_t tok_begin;
+  int32_t ntok;
+  int32_t kvh;
+};
+
+struct BwdTile {
+  int32_t step;     // ring step block j
+  int32_t seq;
+  int32_t kvh;
+  int32_t u0;       // first key, as an index inside the sequence's segment
+  int32_t nk;       // keys in this item (<= kBwdKeys)
+  int32_t q_begin;  // first token that sees at least one of the keys
+  int32_t q_full;   // tokens >= q_full see all of them
+  int32_t q_end;
+};
+
+// Number of keys of ring-step block j (rank j's chunks j and 2C-1-j of a
+// sequence with chunk length c) at positions <= P.  Positions increase with
+// the local index inside the block, so the visible keys are a prefix.
+__host__ __device__ inline int32_t visible_keys(int32_t P, int32_t j, int32_t C, int32_t c) {
+  int32_t a = P - j * c + 1;
+  int32_t b = P - (2 * C - 1 - j) * c + 1;
+  a = a < 0 ? 0 : (a > c ? c : a);
+  b = b < 0 ? 0 : (b > c ? c : b);
+  return a + b;
+}
+
+struct Plan {
+  // problem
+  int32_t num_seqs = 0, cp_size = 1, cp_rank = 0, hq = 0, hkv = 0, head_dim = 0, group = 1;
+  float scale = 0.f;
+  int64_t n_local = 0;
+  int32_t num_branch_rows = 0;
+  bool any_main_query = false;
+  std::vector<int32_t> cu_seqlens;
+  // tables (host copies, uploaded into the workspace per call)
+  std::vector<SeqInfo> seqs;
+  std::vector<TokInfo> toks;
+  std::vector<GroupInfo> groups;
+  std::vector<FwdTile> fwd_tiles;
+  std::vector<BwdTile> bwd_tiles;      // grouped by ring step i = 0..C-1
+  std::vector<int32_t> bwd_step_off;   // [C+1] tile range of each ring step
+  // packed image of the tables and their byte offsets inside it
+  std::vector<uint8_t> image;
+  size_t off_seqs = 0, off_toks = 0, off_groups = 0, off_fwd = 0, off_bwd = 0;
+  // counts
+  double pairs_per_head = 0.0;  // allowed (query, key) pairs per query head
+  int32_t max_group_len = 0;
+};
+
+// workspace layout (byte offsets), computed from a plan
+struct WorkspaceLayout {
+  size_t tables = 0;   // start of the table image
+  size_t o_acc = 0;    // fp32 [T, hq, d]   (per-step forward)
+  size_t lse_acc = 0;  // fp32 [T, hq]      (per-step forward)
+  size_t rowstat = 0;  // float2 [T, hq]    (backward: LSE*log2e, Delta)
+  size_t dq_acc = 0;   // fp32 [T, hq, d]   (backward)
+  size_t fwd_total = 0;
+  size_t bwd_total = 0;
+};
+
+WorkspaceLayout workspace_layout(const Plan& p, int mode);
+
+// thread-local error message
+void set_error(const std::string& msg);
+
+}  // namespace ba
+
+struct ba_plan {
+  ba::Plan p;
+};

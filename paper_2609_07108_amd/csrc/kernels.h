@@ -1,0 +1,84 @@
+// Kernel parameter blocks and launchers (device side of the library).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "ba_internal.h"
+#include "device_common.h"
+
+namespace ba {
+
+constexpr int kMaxCp = 32;  // ring steps whose block pointers fit in a kernel argument
+
+constexpr int kModeStep = 0;   // one ring step, merge into the running pair
+constexpr int kModeFinal = 1;  // branch-local part + merge + write, main part from the running pair
+constexpr int kModeFused = 2;  // every ring step + branch-local part + merge + write
+
+struct FwdParams {
+  const SeqInfo* seqs;
+  const TokInfo* toks;
+  const GroupInfo* groups;
+  const FwdTile* tiles;
+  int32_t num_tiles;
+  int32_t C, rank, hq, hkv, G;
+  float scale_log2;  // softmax scale * log2(e)
+  int64_t n_local;
+  int64_t n_br;
+  const bf16* q_main;
+  const bf16* q_br;
+  const bf16* k_br;
+  const bf16* v_br;
+  const bf16* k_step[kMaxCp];
+  const bf16* v_step[kMaxCp];
+  bf16* o_main;
+  bf16* o_br;
+  float* lse_main;
+  float* lse_br;
+  float* o_acc;    // [T * hq, d] running output (per-step schedule)
+  float* lse_acc;  // [T * hq] running LSE, log2 units
+  int32_t step_first, step_count, acc_first;
+};
+
+struct BwdParams {
+  const SeqInfo* seqs;
+  const TokInfo* toks;
+  const GroupInfo* groups;
+  const BwdTile* tiles;
+  int32_t num_tiles;
+  int32_t C, rank, hq, hkv, G;
+  int32_t num_tokens;
+  int32_t num_groups;
+  float scale;       // softmax scale
+  float scale_log2;  // softmax scale * log2(e)
+  int64_t n_local;
+  int64_t n_br;
+  const bf16* q_main;
+  const bf16* q_br;
+  const bf16* k_br;
+  const bf16* v_br;
+  const bf16* k_step[kMaxCp];
+  const bf16* v_step[kMaxCp];
+  const bf16* o_main;
+  const bf16* o_br;
+  const float* lse_main;
+  const float* lse_br;
+  const bf16* do_main;
+  const bf16* do_br;
+  void* dq_main;
+  void* dq_br;
+  void* dk_step[kMaxCp];
+  void* dv_step[kMaxCp];
+  void* dk_br;
+  void* dv_br;
+  int32_t grad_f32;
+  float2* rowstat;  // [T * hq]: (LSE * log2 e, Delta = <dO, O>)
+  float* dq_acc;    // [T * hq, d], unscaled dS K sums
+};
+
+hipError_t launch_fwd(const FwdParams& p, int mode, hipStream_t stream);
+hipError_t launch_bwd_preprocess(const BwdParams& p, hipStream_t stream);
+hipError_t launch_bwd_main(const BwdParams& p, hipStream_t stream);
+hipError_t launch_bwd_branch(const BwdParams& p, int max_group_len, hipStream_t stream);
+hipError_t launch_bwd_finalize(const BwdParams& p, hipStream_t stream);
+hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+}  // namespace ba

@@ -1,0 +1,326 @@
+// Host planner: zigzag partition, descriptor validation and the work tables
+// the kernels consume.  Host code only (no HIP runtime calls).
+#include <algorithm>
+#include <exception>
+#include <new>
+#include <cmath>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "ba_internal.h"
+
+namespace ba {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+
+static int fail(int code, const std::string& msg) {
+  set_error(msg);
+  return code;
+}
+
+static int check_seqlens(const int32_t* cu, int32_t num_seqs, int32_t cp_size, int32_t cp_rank) {
+  if (!cu) return fail(BA_E_INVAL, "cu_seqlens is NULL");
+  if (num_seqs < 1) return fail(BA_E_INVAL, "num_seqs must be >= 1");
+  if (cp_size < 1) return fail(BA_E_INVAL, "cp_size must be >= 1");
+  if (cp_rank < 0 || cp_rank >= cp_size) return fail(BA_E_INVAL, "cp_rank outside [0, cp_size)");
+  if (cu[0] != 0) return fail(BA_E_INVAL, "cu_seqlens[0] must be 0");
+  for (int32_t s = 0; s < num_seqs; ++s) {
+    int64_t L = (int64_t)cu[s + 1] - cu[s];
+    if (L < 0) return fail(BA_E_INVAL, "cu_seqlens must be non-decreasing");
+    if (L % (2 * (int64_t)cp_size) != 0)
+      return fail(BA_E_INVAL, "sequence " + std::to_string(s) + " length " + std::to_string(L) +
+                                  " is not a multiple of 2*cp_size");
+  }
+  return BA_OK;
+}
+
+WorkspaceLayout workspace_layout(const Plan& p, int mode) {
+  auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  WorkspaceLayout w;
+  size_t T = p.toks.size();
+  size_t rows = T * (size_t)p.hq;
+  size_t off = 0;
+  w.tables = off;
+  off = align(off + p.image.size());
+  size_t after_tables = off;
+  if (mode == BA_MODE_PER_STEP) {
+    w.o_acc = off;
+    off = align(off + rows * kHeadDim * sizeof(float));
+    w.lse_acc = off;
+    off = align(off + rows * sizeof(float));
+  }
+  w.fwd_total = off;
+  off = after_tables;
+  w.rowstat = off;
+  off = align(off + rows * 2 * sizeof(float));
+  w.dq_acc = off;
+  off = align(off + rows * kHeadDim * sizeof(float));
+  w.bwd_total = off;
+  return w;
+}
+
+template <typename T>
+static size_t append(std::vector<uint8_t>& img, const std::vector<T>& v) {
+  size_t off = (img.size() + 255) & ~size_t(255);
+  img.resize(off + v.size() * sizeof(T));
+  if (!v.empty()) std::memcpy(img.data() + off, v.data(), v.size() * sizeof(T));
+  return off;
+}
+
+static int build_plan(const ba_problem* pr, Plan& P) {
+  int rc = check_seqlens(pr->cu_seqlens, pr->num_seqs, pr->cp_size, pr->cp_rank);
+  if (rc) return rc;
+  if (pr->head_dim != kHeadDim)
+    return fail(BA_E_UNSUPPORTED, "head_dim " + std::to_string(pr->head_dim) + " unsupported (only 128)");
+  if (pr->hq < 1 || pr->hkv < 1 || pr->hq % pr->hkv != 0)
+    return fail(BA_E_INVAL, "hq and hkv must be positive with hq % hkv == 0");
+  const int32_t G = pr->hq / pr->hkv;
+  if (G > kBwdRows)
+    return fail(BA_E_UNSUPPORTED, "hq/hkv > " + std::to_string(kBwdRows) + " unsupported");
+  if (!std::isfinite(pr->softmax_scale)) return fail(BA_E_INVAL, "softmax_scale not finite");
+  if (pr->num_groups < 0 || (pr->num_groups > 0 && !pr->groups))
+    return fail(BA_E_INVAL, "groups missing");
+  if (pr->num_branch_rows < 0) return fail(BA_E_INVAL, "num_branch_rows < 0");
+
+  const int32_t S = pr->num_seqs, C = pr->cp_size, r = pr->cp_rank;
+  P.num_seqs = S;
+  P.cp_size = C;
+  P.cp_rank = r;
+  P.hq = pr->hq;
+  P.hkv = pr->hkv;
+  P.group = G;
+  P.head_dim = pr->head_dim;
+  P.scale = pr->softmax_scale;
+  P.num_branch_rows = pr->num_branch_rows;
+  P.cu_seqlens.assign(pr->cu_seqlens, pr->cu_seqlens + S + 1);
+  P.n_local = (int64_t)pr->cu_seqlens[S] / C;
+
+  // --- validate groups
+  std::vector<uint8_t> used((size_t)pr->num_branch_rows, 0);
+  std::vector<std::vector<int32_t>> groups_of_seq(S);
+  for (int32_t g = 0; g < pr->num_groups; ++g) {
+    const ba_group& gr = pr->groups[g];
+    std::string at = "group " + std::to_string(g) + ": ";
+    if (gr.seq < 0 || gr.seq >= S) return fail(BA_E_INVAL, at + "seq out of range");
+    int32_t L = pr->cu_seqlens[gr.seq + 1] - pr->cu_seqlens[gr.seq];
+    if (gr.anchor < 0 || gr.anchor >= L) return fail(BA_E_INVAL, at + "anchor outside the sequence");
+    int32_t c = L / (2 * C);
+    int32_t chunk = gr.anchor / c;
+    int32_t owner = std::min(chunk, 2 * C - 1 - chunk);
+    if (owner != r) return fail(BA_E_INVAL, at + "anchor is owned by rank " + std::to_string(owner));
+    if (gr.kind != BA_KIND_EAGLE_CHAIN && gr.kind != BA_KIND_DFLASH_BLOCK)
+      return fail(BA_E_INVAL, at + "unknown kind");
+    if (gr.len < 1 || gr.len > BA_MAX_GROUP_LEN) return fail(BA_E_INVAL, at + "len outside [1, 64]");
+    if (gr.row_stride < 1) return fail(BA_E_INVAL, at + "row_stride must be >= 1");
+    for (int32_t i = 0; i < gr.len; ++i) {
+      int64_t row = (int64_t)gr.row0 + (int64_t)i * gr.row_stride;
+      if (row < 0 || row >= pr->num_branch_rows) return fail(BA_E_INVAL, at + "member row out of range");
+      if (used[row]) return fail(BA_E_INVAL, at + "member rows overlap another group");
+      used[row] = 1;
+    }
+    groups_of_seq[gr.seq].push_back(g);
+  }
+  P.groups.resize(pr->num_groups);
+  for (int32_t g = 0; g < pr->num_groups; ++g) {
+    P.groups[g] = GroupInfo{pr->groups[g].row0, pr->groups[g].row_stride, pr->groups[g].len,
+                            pr->groups[g].kind, -1, {0, 0, 0}};
+    P.max_group_len = std::max(P.max_group_len, pr->groups[g].len);
+  }
+
+  // --- per sequence: token list ordered by causal limit
+  P.seqs.resize(S);
+  double pairs = 0.0;
+  int64_t local_off = 0;
+  for (int32_t s = 0; s < S; ++s) {
+    int32_t L = pr->cu_seqlens[s + 1] - pr->cu_seqlens[s];
+    int32_t c = L / (2 * C);
+    SeqInfo& si = P.seqs[s];
+    si.seg_off = (int32_t)local_off;
+    si.c = c;
+    si.tok_begin = (int32_t)P.toks.size();
+    std::vector<TokInfo> tk;
+    bool main_q = pr->has_main ? pr->has_main[s] != 0 : true;
+    if (main_q && c > 0) {
+      P.any_main_query = true;
+      for (int32_t u = 0; u < 2 * c; ++u) {
+        int32_t pos = u < c ? r * c + u : (2 * C - 1 - r) * c + (u - c);
+        tk.push_back(TokInfo{(int32_t)(local_off + u), pos, -1, -1});
+      }
+    }
+    for (int32_t g : groups_of_seq[s]) {
+      const ba_group& gr = pr->groups[g];
+      for (int32_t i = 0; i < gr.len; ++i)
+        tk.push_back(TokInfo{-(gr.row0 + i * gr.row_stride) - 1, gr.anchor, g, i});
+    }
+    std::stable_sort(tk.begin(), tk.end(), [](const TokInfo& a, const TokInfo& b) {
+      if (a.P != b.P) return a.P < b.P;
+      if (a.grp != b.grp) return a.grp < b.grp;  // main (-1) first, then by group
+      return a.gidx < b.gidx;
+    });
+    for (const TokInfo& t : tk) {
+      pairs += (double)t.P + 1.0;
+      if (t.grp >= 0) {
+        const ba_group& gr = pr->groups[t.grp];
+        pairs += gr.kind == BA_KIND_EAGLE_CHAIN ? (double)(t.gidx + 1) : (double)gr.len;
+      }
+    }
+    for (size_t i = 0; i < tk.size(); ++i)
+      if (tk[i].grp >= 0 && tk[i].gidx == 0) P.groups[tk[i].grp].tok0 = (int32_t)(P.toks.size() + i);
+    P.toks.insert(P.toks.end(), tk.begin(), tk.end());
+    si.tok_end = (int32_t)P.toks.size();
+    local_off += 2 * c;
+  }
+  P.pairs_per_head = pairs;
+
+  // --- forward tiles: kFwdRows / G tokens x G heads, never across sequences
+  const int32_t tpt = kFwdRows / G;
+  struct Keyed {
+    int64_t work;
+    FwdTile t;
+  };
+  std::vector<Keyed> ft;
+  for (int32_t s = 0; s < S; ++s) {
+    const SeqInfo& si = P.seqs[s];
+    for (int32_t t0 = si.tok_begin; t0 < si.tok_end; t0 += tpt) {
+      int32_t n = std::min(tpt, si.tok_end - t0);
+      int64_t work = (int64_t)P.toks[t0 + n - 1].P + 1;
+      for (int32_t h = 0; h < pr->hkv; ++h) ft.push_back(Keyed{work, FwdTile{s, t0, n, h}});
+    }
+  }
+  // longest first: the causal prefix length is the tile's work
+  std::stable_sort(ft.begin(), ft.end(), [](const Keyed& a, const Keyed& b) { return a.work > b.work; });
+  P.fwd_tiles.reserve(ft.size());
+  for (auto& k : ft) P.fwd_tiles.push_back(k.t);
+
+  // --- backward tiles: kBwdKeys keys of one ring-step block, grouped by ring
+  // step in the order the ring delivers the blocks (step i brings rank
+  // (r - i) mod C), longest first inside a step
+  P.bwd_step_off.assign(C + 1, 0);
+  for (int32_t i = 0; i < C; ++i) {
+    const int32_t j = ((r - i) % C + C) % C;
+    struct KeyedB {
+      int64_t work;
+      BwdTile t;
+    };
+    std::vector<KeyedB> bt;
+    for (int32_t s = 0; s < S; ++s) {
+      const SeqInfo& si = P.seqs[s];
+      if (si.tok_end == si.tok_begin) continue;
+      for (int32_t u0 = 0; u0 < 2 * si.c; u0 += kBwdKeys) {
+        const int32_t nk = std::min(kBwdKeys, 2 * si.c - u0);
+        // tokens are ordered by P and visible_keys is monotone in P
+        auto first_with = [&](int32_t need) {
+          int32_t lo = si.tok_begin, hi = si.tok_end;
+          while (lo < hi) {
+            int32_t mid = lo + (hi - lo) / 2;
+            if (visible_keys(P.toks[mid].P, j, C, si.c) >= need) hi = mid; else lo = mid + 1;
+          }
+          return lo;
+        };
+        const int32_t qb = first_with(u0 + 1);
+        const int32_t qf = first_with(u0 + nk);
+        if (qb == si.tok_end) continue;
+        for (int32_t h = 0; h < pr->hkv; ++h)
+          bt.push_back(KeyedB{(int64_t)(si.tok_end - qb), BwdTile{j, s, h, u0, nk, qb, qf, si.tok_end}});
+      }
+    }
+    std::stable_sort(bt.begin(), bt.end(), [](const KeyedB& a, const KeyedB& b) { return a.work > b.work; });
+    for (auto& k : bt) P.bwd_tiles.push_back(k.t);
+    P.bwd_step_off[i + 1] = (int32_t)P.bwd_tiles.size();
+  }
+
+  // --- packed table image
+  P.image.clear();
+  P.off_seqs = append(P.image, P.seqs);
+  P.off_toks = append(P.image, P.toks);
+  P.off_groups = append(P.image, P.groups);
+  P.off_fwd = append(P.image, P.fwd_tiles);
+  P.off_bwd = append(P.image, P.bwd_tiles);
+  P.image.resize((P.image.size() + 255) & ~size_t(255));
+  return BA_OK;
+}
+
+}  // namespace ba
+
+extern "C" {
+
+const char* branch_attn_last_error(void) { return ba::g_last_error.c_str(); }
+
+int zigzag_partition(const int32_t* cu_seqlens, int32_t num_seqs, int32_t cp_size, int32_t cp_rank,
+                     int32_t* local_cu_seqlens, int32_t* local_to_global, int32_t* local_pos) {
+  int rc = ba::check_seqlens(cu_seqlens, num_seqs, cp_size, cp_rank);
+  if (rc) return rc;
+  if (!local_cu_seqlens || !local_to_global || !local_pos)
+    return ba::fail(BA_E_INVAL, "output arrays must not be NULL");
+  const int32_t C = cp_size, r = cp_rank;
+  int64_t out = 0;
+  local_cu_seqlens[0] = 0;
+  for (int32_t s = 0; s < num_seqs; ++s) {
+    int32_t L = cu_seqlens[s + 1] - cu_seqlens[s];
+    int32_t c = L / (2 * C);
+    for (int32_t half = 0; half < 2; ++half) {
+      int32_t chunk = half == 0 ? r : 2 * C - 1 - r;
+      for (int32_t i = 0; i < c; ++i) {
+        int32_t pos = chunk * c + i;
+        local_pos[out] = pos;
+        local_to_global[out] = cu_seqlens[s] + pos;
+        ++out;
+      }
+    }
+    local_cu_seqlens[s + 1] = (int32_t)out;
+  }
+  return BA_OK;
+}
+
+int branch_attn_plan_create(const ba_problem* prob, ba_plan** out) {
+  if (!out) return ba::fail(BA_E_INVAL, "out is NULL");
+  *out = nullptr;
+  if (!prob) return ba::fail(BA_E_INVAL, "problem is NULL");
+  ba_plan* p = new (std::nothrow) ba_plan();
+  if (!p) return ba::fail(BA_E_INVAL, "out of host memory");
+  int rc;
+  try {
+    rc = ba::build_plan(prob, p->p);
+  } catch (const std::exception& e) {
+    rc = ba::fail(BA_E_INVAL, std::string("plan construction failed: ") + e.what());
+  }
+  if (rc) {
+    delete p;
+    return rc;
+  }
+  *out = p;
+  return BA_OK;
+}
+
+void branch_attn_plan_destroy(ba_plan* plan) { delete plan; }
+
+int branch_attn_workspace_size(const ba_plan* plan, int32_t mode, size_t* fwd_bytes, size_t* bwd_bytes) {
+  if (!plan) return ba::fail(BA_E_INVAL, "plan is NULL");
+  if (mode != BA_MODE_PER_STEP && mode != BA_MODE_FUSED) return ba::fail(BA_E_INVAL, "unknown mode");
+  ba::WorkspaceLayout w = ba::workspace_layout(plan->p, mode);
+  if (fwd_bytes) *fwd_bytes = w.fwd_total;
+  if (bwd_bytes) *bwd_bytes = w.bwd_total;
+  return BA_OK;
+}
+
+int branch_attn_plan_info(const ba_plan* plan, int64_t* n_local, int64_t* n_query_tokens) {
+  if (!plan) return ba::fail(BA_E_INVAL, "plan is NULL");
+  if (n_local) *n_local = plan->p.n_local;
+  if (n_query_tokens) *n_query_tokens = (int64_t)plan->p.toks.size();
+  return BA_OK;
+}
+
+int branch_attn_useful_flops(const ba_plan* plan, double* fwd_flops, double* bwd_flops) {
+  if (!plan) return ba::fail(BA_E_INVAL, "plan is NULL");
+  const ba::Plan& p = plan->p;
+  double per = p.pairs_per_head * p.hq * p.head_dim;
+  if (fwd_flops) *fwd_flops = 4.0 * per;
+  if (bwd_flops) *bwd_flops = 10.0 * per;
+  return BA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,167 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
+same seeded bf16 inputs, element by element.
+
+The cases span several query and key tiles with ragged tails, every GQA
+ratio the kernels tile differently (G = 1, 4, 8, 16), both branch kinds,
+both branch-array layouts, both ring schedules, context-parallel ranks at
+either end of the ring, an empty sequence, sequences without branches, fp32
+gradient output, and all-equal scores (Q = 0).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_07108_amd import binding as B
+from paper_2609_07108_amd import rankshare as RS
+from paper_2609_07108_amd import workloads as W
+from tests import gpu_helpers as H
+
+pytestmark = pytest.mark.gpu
+
+MODES = {"per_step": B.BA_MODE_PER_STEP, "fused": B.BA_MODE_FUSED}
+
+
+def case(name):
+    if name == "eagle_varlen_cp4":
+        return W.custom([1152, 520, 264], [("eagle", 7)] * 3, hq=32, hkv=8, cp_size=4, cp_rank=0,
+                        seed=201, name=name)
+    if name == "eagle_varlen_cp4_last_rank":
+        return W.custom([1152, 520, 264], [("eagle", 3)] * 3, hq=32, hkv=8, cp_size=4, cp_rank=3,
+                        seed=202, name=name)
+    if name == "dflash_g8":
+        return W.custom([2048], [("dflash", 16, 64)], hq=64, hkv=8, cp_size=1, cp_rank=0, seed=203,
+                        name=name)
+    if name == "mixed_g16":
+        return W.custom([768, 1024, 384, 512], [("eagle", 5), ("dflash", 16, 64)] * 2, hq=16, hkv=1,
+                        cp_size=4, cp_rank=3, seed=204, name=name)
+    if name == "edge_g1":
+        return W.custom([0, 64, 8, 16], [None, ("eagle", 1), ("eagle", 2), None], hq=2, hkv=2,
+                        cp_size=2, cp_rank=1, seed=205, name=name)
+    raise KeyError(name)
+
+
+@pytest.fixture(scope="module")
+def cuda():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+    return torch.device("cuda:0")
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+@pytest.mark.parametrize("r", [0, 1, 2, 3])
+def test_config1_forward_every_rank(cuda, mode, r):
+    prob = W.config(1).with_rank(r)
+    t = H.oracle_inputs(prob)
+    mq, bq, ref, _ = H.oracle_run(prob, t, backward=False)
+    share = RS.build_share(prob, device="cuda")
+    got, _ = H.gpu_fwd(share, MODES[mode], mq, bq)
+    H.assert_fwd_close(got, ref)
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+@pytest.mark.parametrize("name,layout,grad_dtype", [
+    ("eagle_varlen_cp4", "group", torch.bfloat16),
+    ("eagle_varlen_cp4_last_rank", "depth", torch.bfloat16),
+    ("dflash_g8", "group", torch.bfloat16),
+    ("mixed_g16", "depth", torch.bfloat16),
+    ("edge_g1", "group", torch.float32),
+])
+def test_forward_backward_parity(cuda, mode, name, layout, grad_dtype):
+    prob = case(name)
+    t = H.oracle_inputs(prob)
+    mq, bq, ref_f, ref_b = H.oracle_run(prob, t, backward=True)
+    share = RS.build_share(prob, device="cuda", layout=layout)
+    got_f, got_b, _ = H.gpu_bwd(share, MODES[mode], mq, bq, grad_dtype=grad_dtype)
+    H.assert_fwd_close(got_f, ref_f)
+    H.assert_bwd_close(got_b, ref_b)
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+def test_all_equal_scores(cuda, mode):
+    """Q = 0: every allowed score ties; LSE = ln(#keys) exactly in the oracle."""
+    prob = case("mixed_g16")
+    t = H.oracle_inputs(prob, zero_q=True)
+    mq, bq, ref_f, ref_b = H.oracle_run(prob, t, backward=True)
+    share = RS.build_share(prob, device="cuda", zero_q=True)
+    got_f, got_b, _ = H.gpu_bwd(share, MODES[mode], mq, bq)
+    H.assert_fwd_close(got_f, ref_f)
+    H.assert_bwd_close(got_b, ref_b)
+
+
+def test_forward_is_bitwise_repeatable(cuda):
+    prob = case("eagle_varlen_cp4")
+    share = RS.build_share(prob, device="cuda", with_grad=False)
+    mq = np.zeros(0, np.int64)
+    out1 = RS.alloc_outputs(share)
+    out2 = RS.alloc_outputs(share)
+    ws = RS.workspace(share, B.BA_MODE_FUSED)
+    RS.run_fwd(share, out1, B.BA_MODE_FUSED, ws)
+    RS.run_fwd(share, out2, B.BA_MODE_FUSED, ws)
+    torch.cuda.synchronize()
+    for k in ("o_main", "o_br", "lse_main", "lse_br"):
+        assert torch.equal(out1[k], out2[k]), k
+
+
+def test_per_step_and_fused_agree(cuda):
+    prob = case("eagle_varlen_cp4")
+    share = RS.build_share(prob, device="cuda", with_grad=False)
+    outs = []
+    for mode in (B.BA_MODE_PER_STEP, B.BA_MODE_FUSED):
+        out = RS.alloc_outputs(share)
+        RS.run_fwd(share, out, mode, RS.workspace(share, mode))
+        outs.append(out)
+    torch.cuda.synchronize()
+    for k in ("o_main", "o_br"):
+        d = (outs[0][k].float() - outs[1][k].float()).abs().max().item()
+        assert d <= 2 * 2.0 ** -8, (k, d)
+    for k in ("lse_main", "lse_br"):
+        d = (outs[0][k] - outs[1][k]).abs().max().item()
+        assert d <= 1e-4, (k, d)
+
+
+def test_lse_merge_kernel(cuda):
+    """Standalone Eq. lse-merge kernel against the oracle's merge, with empty
+    partials (LSE = -inf) on either side and on both."""
+    import oracle
+    rng = np.random.default_rng(7)
+    rows, heads, d = 1000, 5, 128
+    oa = rng.standard_normal((rows, heads, d)).astype(np.float32)
+    ob = rng.standard_normal((rows, heads, d)).astype(np.float32)
+    la = (rng.standard_normal((heads, rows)) * 4).astype(np.float32)
+    lb = (rng.standard_normal((heads, rows)) * 4).astype(np.float32)
+    la[0, :50] = -np.inf
+    lb[1, 20:80] = -np.inf
+    la[2, :10] = -np.inf
+    lb[2, :10] = -np.inf
+    ob_bf = torch.from_numpy(ob).to(torch.bfloat16)
+    ref_o, ref_l = oracle.lse_merge(oa, la, ob_bf.float().numpy(), lb)
+    for part in (ob_bf, torch.from_numpy(ob)):
+        o_acc = torch.from_numpy(oa).cuda()
+        l_acc = torch.from_numpy(la).cuda()
+        B.lse_merge(o_acc, l_acc, part.cuda(), torch.from_numpy(lb).cuda())
+        torch.cuda.synchronize()
+        ro = ref_o if part.dtype == torch.bfloat16 else oracle.lse_merge(oa, la, ob, lb)[0]
+        np.testing.assert_allclose(o_acc.cpu().numpy(), ro, atol=1e-5, rtol=1e-5)
+        got_l = l_acc.cpu().numpy()
+        assert np.array_equal(np.isneginf(got_l), np.isneginf(ref_l))
+        fin = np.isfinite(ref_l)
+        np.testing.assert_allclose(got_l[fin], ref_l[fin], atol=1e-5, rtol=1e-6)
+        assert np.all(o_acc.cpu().numpy()[np.isneginf(ref_l).T] == 0)
+
+
+def test_errors_do_not_launch(cuda):
+    prob = case("edge_g1")
+    share = RS.build_share(prob, device="cuda")
+    out = RS.alloc_outputs(share)
+    small = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(B.BranchAttnError) as e:
+        RS.run_fwd(share, out, B.BA_MODE_FUSED, small)
+    assert e.value.code == B.BA_E_WORKSPACE
+    misaligned = out["o_main"].view(-1)[1:]
+    with pytest.raises(B.BranchAttnError) as e:
+        B.branch_attn_fwd(share.plan, B.BA_MODE_FUSED, share.t["q_main"], share.t["q_br"], share.t["k_br"],
+                          share.t["v_br"], share.t["k_step"], share.t["v_step"], misaligned, out["o_br"],
+                          out["lse_main"], out["lse_br"], RS.workspace(share, B.BA_MODE_FUSED))
+    assert e.value.code == B.BA_E_INVAL
