@@ -1,0 +1,223 @@
+"""Benchmark: forward + backward branch attention of one context-parallel rank
+share on one MI355X, through the C ABI.
+
+One step = branch_attn_fwd + branch_attn_bwd over the whole rank share (every
+ring step's main-prefix attention, the branch-local attention and the LSE
+merge, then the replayed backward), inputs resident in HBM.
+
+Default workload: one 262144-token sequence, 32 query / 8 KV heads,
+head_dim 128, EAGLE-3 chains of depth 3, the zigzag share of rank 0 at CP = 8
+(32768 main + 98304 branch queries against 262144 main keys), bf16 inputs
+with fp32 accumulation.
+
+Prints ONE JSON line.  `value` is useful TFLOP/s of the whole step (allowed
+query-key pairs x heads x 14 d, forward 4d + backward 10d).  `roofline`
+describes the dominant kernel (timed live with HIP events recorded by the
+library around its ring-kernel launches); `cpu_baseline` is the fp64 CPU
+oracle timed on a bounded sample of query rows of the same share.
+"""
+
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/clk x 2.4 GHz
+PEAK_HBM_GBS = 8000.0
+METRIC = "branch-attn fwd+bwd ms & TFLOP/s (% bf16 MFMA peak), 256K-token rank share"
+
+
+class HipEvents:
+    """Raw hipEvent_t handles from the HIP runtime torch already loaded."""
+
+    def __init__(self):
+        self.h = ctypes.CDLL("libamdhip64.so.7")
+        self.h.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+
+    def create(self):
+        ev = ctypes.c_void_p()
+        rc = self.h.hipEventCreate(ctypes.byref(ev))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed ({rc})")
+        return ev
+
+    def record(self, ev, stream):
+        rc = self.h.hipEventRecord(ev, ctypes.c_void_p(stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def ms(self, a, b):
+        out = ctypes.c_float()
+        rc = self.h.hipEventElapsedTime(ctypes.byref(out), a, b)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return out.value
+
+
+def cpu_baseline(prob, rows: int, seed: int = 1234):
+    """Time the fp64 oracle on `rows` query rows of the share (fwd + bwd)."""
+    import numpy as np
+    import oracle
+
+    mq, bq = oracle.select_queries(prob)
+    rng = np.random.default_rng(seed)
+    n_m = max(1, rows // 4)
+    sm = np.sort(rng.choice(mq, size=min(n_m, len(mq)), replace=False)) if len(mq) else mq[:0]
+    sb = np.sort(rng.choice(bq, size=min(rows - len(sm), len(bq)), replace=False)) if len(bq) else bq[:0]
+    H, Hk, d = prob.hq, prob.hkv, prob.head_dim
+
+    def sparse(name, sel, total, heads):
+        a = np.zeros((total, heads, d), np.float32)  # untouched pages stay unallocated
+        if len(sel):
+            a[sel] = prob.draw(name, sel).float().numpy()
+        return a
+
+    # branch keys the sampled rows can reach: every member of their groups
+    grp = np.repeat(np.arange(len(prob.g_len)), prob.g_len)
+    gsel = np.unique(grp[sb]) if len(sb) else np.zeros(0, np.int64)
+    brows = np.concatenate([np.arange(prob.g_row0[g], prob.g_row0[g] + prob.g_len[g]) for g in gsel]) \
+        if len(gsel) else np.zeros(0, np.int64)
+    t = dict(qm=sparse("qm", sm, prob.n_main, H), qb=sparse("qb", sb, prob.n_branch, H),
+             km=prob.draw("km").float().numpy(), vm=prob.draw("vm").float().numpy(),
+             kb=sparse("kb", brows, prob.n_branch, Hk), vb=sparse("vb", brows, prob.n_branch, Hk))
+    dom = prob.draw("dom", sm).float().numpy() if len(sm) else np.zeros((0, H, d), np.float32)
+    dob = prob.draw("dob", sb).float().numpy() if len(sb) else np.zeros((0, H, d), np.float32)
+    args = [t[k] for k in ("qm", "km", "vm", "qb", "kb", "vb")]
+    t0 = time.perf_counter()
+    oracle.forward(prob, *args, sm, sb)
+    oracle.backward(prob, *args, dom, dob, sm, sb)
+    dt = time.perf_counter() - t0
+    pm, pl = oracle.allowed_pair_counts(prob, sm, sb)
+    f_fwd, f_bwd = oracle.useful_flops(prob, pm + pl)
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    return {"value": (f_fwd + f_bwd) / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{len(sm)} main + {len(sb)} branch query rows of the share, fp64 fwd+bwd against "
+                      f"all their keys, {dt:.1f} s", "seconds": round(dt, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=4, help="named workload 1..5 (4 = 256K headline)")
+    ap.add_argument("--mode", choices=["fused", "per_step"], default="fused")
+    ap.add_argument("--cpu-rows", type=int, default=24, help="oracle sample size (0 disables)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build evaluates one context-parallel rank share on ONE GPU; "
+                                   "--gpus > 1 is not supported (the ring exchange is not implemented)"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2609_07108_amd import binding as B
+    from paper_2609_07108_amd import rankshare as RS
+    from paper_2609_07108_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    prob = W.config(args.config)
+    mode = B.BA_MODE_FUSED if args.mode == "fused" else B.BA_MODE_PER_STEP
+    t0 = time.perf_counter()
+    share = RS.build_share(prob, device="cuda:0", with_grad=True)
+    out = RS.alloc_outputs(share, grads=True)
+    ws = RS.workspace(share, mode, backward=True)
+    torch.cuda.synchronize()
+    print(f"[bench] inputs ready in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    f_fwd, f_bwd = share.plan.useful_flops()
+    main_pairs, local_pairs = share.plan.pair_counts()
+    d, hq = prob.head_dim, prob.hq
+    ring_fwd_flops = main_pairs * hq * 4 * d
+    ring_bwd_flops = main_pairs * hq * 10 * d
+
+    ev = HipEvents()
+    stream = torch.cuda.current_stream().cuda_stream
+    fb, fe, bb, be, bk = [], [], [], [], []
+
+    def step(i=None):
+        evf = (fb[i], fe[i]) if i is not None else (None, None)
+        evb = (bb[i], be[i], bk[i]) if i is not None else (None, None, None)
+        RS.run_fwd(share, out, mode, ws, ring_events=evf)
+        RS.run_bwd(share, out, mode, ws, ring_events=evb)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+    for _ in range(args.steps):
+        fb.append(ev.create()); fe.append(ev.create()); bb.append(ev.create()); be.append(ev.create())
+        bk.append(ev.create())
+    start, stop = ev.create(), ev.create()
+    torch.cuda.synchronize()
+    ev.record(start, stream)
+    for i in range(args.steps):
+        step(i)
+    ev.record(stop, stream)
+    torch.cuda.synchronize()
+    total_ms = ev.ms(start, stop)
+    ms_step = total_ms / args.steps
+    fwd_ring_ms = sum(ev.ms(a, b) for a, b in zip(fb, fe)) / args.steps
+    bwd_ring_ms = sum(ev.ms(a, b) for a, b in zip(bb, be)) / args.steps
+    kern = {"fwd_kernel": (fwd_ring_ms, ring_fwd_flops)}
+    if mode == B.BA_MODE_FUSED:
+        # the backward ring part is two kernels: dK/dV (S, dP, dV, dK: 8d per
+        # pair) then dQ (S, dP, dQ: 6d per pair)
+        kv_ms = sum(ev.ms(a, b) for a, b in zip(bb, bk)) / args.steps
+        kern["bwd_kv_kernel"] = (kv_ms, main_pairs * hq * 8 * d)
+        kern["bwd_dq_kernel"] = (bwd_ring_ms - kv_ms, main_pairs * hq * 6 * d)
+    else:
+        kern["bwd ring (dK/dV + dQ)"] = (bwd_ring_ms, main_pairs * hq * 14 * d)
+    print(f"[bench] {args.steps} steps: {ms_step:.2f} ms/step; " +
+          ", ".join(f"{k} {v[0]:.2f} ms ({v[1] / v[0] / 1e9:.0f} TFLOP/s)" for k, v in kern.items()),
+          file=sys.stderr, flush=True)
+
+    launches = 1 if mode == B.BA_MODE_FUSED else prob.cp_size
+    dom_name = max(kern, key=lambda k: kern[k][0])
+    dom_ms, dom_flops = kern[dom_name]
+    achieved = dom_flops / (dom_ms / 1e3) / 1e12
+    value = (f_fwd + f_bwd) / (ms_step / 1e3) / 1e12
+
+    cpu = None
+    if args.cpu_rows > 0:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(prob, args.cpu_rows)
+
+    n_local, ntok = share.plan.info()
+    line = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": prob.name, "describe": prob.describe, "mode": args.mode,
+                   "query_rows": ntok, "main_keys": prob.n_main, "hq": prob.hq, "hkv": prob.hkv,
+                   "head_dim": d, "cp_size": prob.cp_size, "cp_rank": prob.cp_rank},
+        "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "useful_tflop_per_step": {"fwd": round(f_fwd / 1e12, 3), "bwd": round(f_bwd / 1e12, 3)},
+        "ring_ms": {"fwd": round(fwd_ring_ms, 3), "bwd": round(bwd_ring_ms, 3)},
+        "kernels": {k: {"ms": round(v[0], 3), "tflops": round(v[1] / v[0] / 1e9, 1)} for k, v in kern.items()},
+        "roofline": {"kernel": dom_name, "bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": round(PEAK_BF16_TFLOPS, 1), "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "launches_per_step": launches},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

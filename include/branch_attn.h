@@ -116,7 +116,10 @@ typedef struct ba_problem {
  * queries are left untouched), o_br [num_branch_rows, hq, d] bf16, lse_main
  * [hq, n_local], lse_br [hq, num_branch_rows] fp32 (natural log).  Rows of
  * the branch arrays not covered by any group are neither read nor written.
- * Pointers may be NULL when the corresponding row count is 0. */
+ * Pointers may be NULL when the corresponding row count is 0.
+ * ring_begin / ring_end: optional hipEvent_t (NULL = none), recorded on the
+ * call's stream right before the first and right after the last launch of the
+ * main-sequence (ring) kernels, so a caller can time that part alone. */
 typedef struct ba_fwd_io {
   const void* q_main;
   const void* q_br;
@@ -128,6 +131,8 @@ typedef struct ba_fwd_io {
   void* o_br;
   float* lse_main;
   float* lse_br;
+  void* ring_begin;
+  void* ring_end;
 } ba_fwd_io;
 
 /* Device pointers of one backward call.  Inputs as in ba_fwd_io plus the
@@ -136,7 +141,9 @@ typedef struct ba_fwd_io {
  * accumulated): dq_main / dq_br like q_*, dk_step[j] / dv_step[j] like
  * k_step[j] (the gradient contributed by THIS rank's queries to rank j's
  * block; a real ring returns it to rank j), dk_br / dv_br like k_br.  The
- * LSE outputs receive no gradient. */
+ * LSE outputs receive no gradient.  ring_begin / ring_end as in ba_fwd_io;
+ * kv_end (optional hipEvent_t) is recorded in BA_MODE_FUSED between the
+ * dK/dV launch and the dQ launch of the ring part, and ignored otherwise. */
 typedef struct ba_bwd_io {
   const void* q_main;
   const void* q_br;
@@ -157,6 +164,9 @@ typedef struct ba_bwd_io {
   void* dk_br;
   void* dv_br;
   int32_t grad_dtype;  /* BA_DTYPE_BF16 or BA_DTYPE_F32 */
+  void* ring_begin;
+  void* ring_end;
+  void* kv_end;
 } ba_bwd_io;
 
 typedef struct ba_plan ba_plan; /* opaque, host-side */
@@ -198,6 +208,11 @@ int branch_attn_plan_info(const ba_plan* plan, int64_t* n_local, int64_t* n_quer
  * 10*head_dim (QK^T recompute, dP, dV, dK, dQ) backward.  Work spent on
  * masked-out pairs inside partial tiles is not counted. */
 int branch_attn_useful_flops(const ba_plan* plan, double* fwd_flops, double* bwd_flops);
+
+/* Allowed (query, key) pairs per query head, split into the causal
+ * main-sequence prefix (computed by the ring kernels) and the branch-local
+ * keys. */
+int branch_attn_pair_counts(const ba_plan* plan, double* main_pairs, double* local_pairs);
 
 /* Message for the last non-OK status returned on this thread. */
 const char* branch_attn_last_error(void);

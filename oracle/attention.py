@@ -142,7 +142,7 @@ def _mask(sp, qsel):
 
 
 def _gather(t, rows):
-    return np.asarray(t, dtype=np.float64)[rows]
+    return np.asarray(t)[rows].astype(np.float64)
 
 
 # ----------------------------------------------------------------------

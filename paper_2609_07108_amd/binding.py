@@ -32,7 +32,8 @@ BA_MODE_FUSED = 1
 
 EXPORTED = ("zigzag_partition", "branch_attn_plan_create", "branch_attn_plan_destroy",
             "branch_attn_workspace_size", "branch_attn_plan_info", "branch_attn_useful_flops",
-            "branch_attn_last_error", "branch_attn_fwd", "branch_attn_bwd", "lse_merge")
+            "branch_attn_pair_counts", "branch_attn_last_error", "branch_attn_fwd", "branch_attn_bwd",
+            "lse_merge")
 
 c_i32 = ctypes.c_int32
 c_vp = ctypes.c_void_p
@@ -53,7 +54,8 @@ class BaProblem(ctypes.Structure):
 class BaFwdIO(ctypes.Structure):
     _fields_ = [("q_main", c_vp), ("q_br", c_vp), ("k_br", c_vp), ("v_br", c_vp),
                 ("k_step", ctypes.POINTER(c_vp)), ("v_step", ctypes.POINTER(c_vp)),
-                ("o_main", c_vp), ("o_br", c_vp), ("lse_main", c_vp), ("lse_br", c_vp)]
+                ("o_main", c_vp), ("o_br", c_vp), ("lse_main", c_vp), ("lse_br", c_vp),
+                ("ring_begin", c_vp), ("ring_end", c_vp)]
 
 
 class BaBwdIO(ctypes.Structure):
@@ -62,7 +64,8 @@ class BaBwdIO(ctypes.Structure):
                 ("o_main", c_vp), ("o_br", c_vp), ("lse_main", c_vp), ("lse_br", c_vp),
                 ("do_main", c_vp), ("do_br", c_vp), ("dq_main", c_vp), ("dq_br", c_vp),
                 ("dk_step", ctypes.POINTER(c_vp)), ("dv_step", ctypes.POINTER(c_vp)),
-                ("dk_br", c_vp), ("dv_br", c_vp), ("grad_dtype", c_i32)]
+                ("dk_br", c_vp), ("dv_br", c_vp), ("grad_dtype", c_i32), ("ring_begin", c_vp),
+                ("ring_end", c_vp), ("kv_end", c_vp)]
 
 
 class BranchAttnError(RuntimeError):
@@ -91,6 +94,8 @@ def lib() -> ctypes.CDLL:
         L.branch_attn_plan_info.argtypes = [c_vp, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
         L.branch_attn_useful_flops.argtypes = [c_vp, ctypes.POINTER(ctypes.c_double),
                                                ctypes.POINTER(ctypes.c_double)]
+        L.branch_attn_pair_counts.argtypes = [c_vp, ctypes.POINTER(ctypes.c_double),
+                                              ctypes.POINTER(ctypes.c_double)]
         L.branch_attn_last_error.restype = ctypes.c_char_p
         L.branch_attn_fwd.argtypes = [c_vp, c_vp, c_i32, ctypes.POINTER(BaFwdIO), c_vp, ctypes.c_size_t]
         L.branch_attn_bwd.argtypes = [c_vp, c_vp, c_i32, ctypes.POINTER(BaBwdIO), c_vp, ctypes.c_size_t]
@@ -174,6 +179,11 @@ class Plan:
         _check(lib().branch_attn_plan_info(self._h, ctypes.byref(n), ctypes.byref(t)))
         return n.value, t.value
 
+    def pair_counts(self):
+        m, l = ctypes.c_double(), ctypes.c_double()
+        _check(lib().branch_attn_pair_counts(self._h, ctypes.byref(m), ctypes.byref(l)))
+        return m.value, l.value
+
     def useful_flops(self):
         f, b = ctypes.c_double(), ctypes.c_double()
         _check(lib().branch_attn_useful_flops(self._h, ctypes.byref(f), ctypes.byref(b)))
@@ -183,22 +193,23 @@ class Plan:
 # --------------------------------------------------------------- device calls
 
 def branch_attn_fwd(plan: Plan, mode: int, q_main, q_br, k_br, v_br, k_step, v_step, o_main, o_br,
-                    lse_main, lse_br, workspace, stream=None):
+                    lse_main, lse_br, workspace, stream=None, ring_events=(None, None)):
     ks, vs = _ptr_array(k_step), _ptr_array(v_step)
     io = BaFwdIO(_ptr(q_main), _ptr(q_br), _ptr(k_br), _ptr(v_br), ks, vs, _ptr(o_main), _ptr(o_br),
-                 _ptr(lse_main), _ptr(lse_br))
+                 _ptr(lse_main), _ptr(lse_br), ring_events[0], ring_events[1])
     _check(lib().branch_attn_fwd(_stream(stream), plan.handle, int(mode), ctypes.byref(io),
                                  _ptr(workspace), workspace.numel() * workspace.element_size()))
 
 
 def branch_attn_bwd(plan: Plan, mode: int, q_main, q_br, k_br, v_br, k_step, v_step, o_main, o_br,
                     lse_main, lse_br, do_main, do_br, dq_main, dq_br, dk_step, dv_step, dk_br, dv_br,
-                    grad_dtype: int, workspace, stream=None):
+                    grad_dtype: int, workspace, stream=None, ring_events=(None, None)):
     ks, vs = _ptr_array(k_step), _ptr_array(v_step)
     dks, dvs = _ptr_array(dk_step), _ptr_array(dv_step)
     io = BaBwdIO(_ptr(q_main), _ptr(q_br), _ptr(k_br), _ptr(v_br), ks, vs, _ptr(o_main), _ptr(o_br),
                  _ptr(lse_main), _ptr(lse_br), _ptr(do_main), _ptr(do_br), _ptr(dq_main), _ptr(dq_br),
-                 dks, dvs, _ptr(dk_br), _ptr(dv_br), int(grad_dtype))
+                 dks, dvs, _ptr(dk_br), _ptr(dv_br), int(grad_dtype), ring_events[0], ring_events[1],
+                 ring_events[2] if len(ring_events) > 2 else None)
     _check(lib().branch_attn_bwd(_stream(stream), plan.handle, int(mode), ctypes.byref(io),
                                  _ptr(workspace), workspace.numel() * workspace.element_size()))
 

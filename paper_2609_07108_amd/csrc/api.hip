@@ -17,6 +17,10 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(BA_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+hipError_t record(void* ev, hipStream_t stream) {
+  return ev ? hipEventRecord(reinterpret_cast<hipEvent_t>(ev), stream) : hipSuccess;
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 // every device tensor is read in 16-byte vectors
@@ -122,10 +126,12 @@ extern "C" int branch_attn_fwd(void* stream_, const ba_plan* plan, int32_t mode,
   p.lse_main = io->lse_main;
   p.lse_br = io->lse_br;
   hipError_t e;
+  if ((e = record(io->ring_begin, stream)) != hipSuccess) return hip_fail(e, "event record");
   if (mode == BA_MODE_FUSED) {
     p.step_first = 0;
     p.step_count = P.cp_size;
     if ((e = launch_fwd(p, kModeFused, stream)) != hipSuccess) return hip_fail(e, "forward launch");
+    if ((e = record(io->ring_end, stream)) != hipSuccess) return hip_fail(e, "event record");
     return BA_OK;
   }
   p.o_acc = reinterpret_cast<float*>(c.ws + c.w.o_acc);
@@ -136,6 +142,7 @@ extern "C" int branch_attn_fwd(void* stream_, const ba_plan* plan, int32_t mode,
     p.acc_first = i == 0;
     if ((e = launch_fwd(p, kModeStep, stream)) != hipSuccess) return hip_fail(e, "ring-step launch");
   }
+  if ((e = record(io->ring_end, stream)) != hipSuccess) return hip_fail(e, "event record");
   p.step_first = 0;
   p.step_count = 0;
   if ((e = launch_fwd(p, kModeFinal, stream)) != hipSuccess) return hip_fail(e, "branch/merge launch");
@@ -192,6 +199,8 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
   p.toks = reinterpret_cast<const TokInfo*>(c.ws + c.w.tables + P.off_toks);
   p.groups = reinterpret_cast<const GroupInfo*>(c.ws + c.w.tables + P.off_groups);
   const BwdTile* tiles = reinterpret_cast<const BwdTile*>(c.ws + c.w.tables + P.off_bwd);
+  p.qtiles = reinterpret_cast<const FwdTile*>(c.ws + c.w.tables + P.off_fwd);
+  p.num_qtiles = (int32_t)P.fwd_tiles.size();
   p.C = P.cp_size;
   p.rank = P.cp_rank;
   p.hq = P.hq;
@@ -219,23 +228,38 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
   p.dv_br = io->dv_br;
   p.grad_f32 = io->grad_dtype == BA_DTYPE_F32;
   p.rowstat = reinterpret_cast<float2*>(c.ws + c.w.rowstat);
-  p.dq_acc = reinterpret_cast<float*>(c.ws + c.w.dq_acc);
+  p.dq_acc = mode == BA_MODE_PER_STEP ? reinterpret_cast<float*>(c.ws + c.w.dq_acc) : nullptr;
 
   if ((e = launch_bwd_preprocess(p, stream)) != hipSuccess) return hip_fail(e, "preprocess launch");
+  if ((e = record(io->ring_begin, stream)) != hipSuccess) return hip_fail(e, "event record");
   if (mode == BA_MODE_FUSED) {
+    // dK/dV of every ring-step block in one launch, then dQ over every step
     p.tiles = tiles;
     p.num_tiles = (int32_t)P.bwd_tiles.size();
-    if ((e = launch_bwd_main(p, stream)) != hipSuccess) return hip_fail(e, "backward launch");
+    if ((e = launch_bwd_kv(p, stream)) != hipSuccess) return hip_fail(e, "dK/dV launch");
+    if ((e = record(io->kv_end, stream)) != hipSuccess) return hip_fail(e, "event record");
+    p.step_first = 0;
+    p.step_count = P.cp_size;
+    if ((e = launch_bwd_dq(p, kModeFused, stream)) != hipSuccess) return hip_fail(e, "dQ launch");
+    if ((e = record(io->ring_end, stream)) != hipSuccess) return hip_fail(e, "event record");
   } else {
+    // ring replay: per step, dK/dV of the arriving block and this rank's dQ sums
     for (int i = 0; i < P.cp_size; ++i) {
       p.tiles = tiles + P.bwd_step_off[i];
       p.num_tiles = P.bwd_step_off[i + 1] - P.bwd_step_off[i];
-      if ((e = launch_bwd_main(p, stream)) != hipSuccess) return hip_fail(e, "ring-step backward launch");
+      if ((e = launch_bwd_kv(p, stream)) != hipSuccess) return hip_fail(e, "ring-step dK/dV launch");
+      p.step_first = i;
+      p.step_count = 1;
+      p.acc_first = i == 0;
+      if ((e = launch_bwd_dq(p, kModeStep, stream)) != hipSuccess) return hip_fail(e, "ring-step dQ launch");
     }
+    if ((e = record(io->ring_end, stream)) != hipSuccess) return hip_fail(e, "event record");
+    p.step_first = 0;
+    p.step_count = 0;
+    if ((e = launch_bwd_dq(p, kModeFinal, stream)) != hipSuccess) return hip_fail(e, "dQ finalize launch");
   }
   if (has_br) {
     if ((e = launch_bwd_branch(p, P.max_group_len, stream)) != hipSuccess) return hip_fail(e, "branch backward launch");
   }
-  if ((e = launch_bwd_finalize(p, stream)) != hipSuccess) return hip_fail(e, "finalize launch");
   return BA_OK;
 }

@@ -22,7 +22,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/branch_attn.h"
+#include "branch_attn.h"
 
 namespace ba {
 
@@ -105,6 +105,7 @@ struct Plan {
   size_t off_seqs = 0, off_toks = 0, off_groups = 0, off_fwd = 0, off_bwd = 0;
   // counts
   double pairs_per_head = 0.0;  // allowed (query, key) pairs per query head
+  double main_pairs_per_head = 0.0;   // ... of which on the causal main prefix
   int32_t max_group_len = 0;
 };
 

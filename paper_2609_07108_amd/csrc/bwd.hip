@@ -2,22 +2,26 @@
 // the backward pass replays the same KV ring and accumulates gradients
 // locally).
 //
-// Using the final LSE of every row, the probabilities of any key set are
-// P = exp(S - LSE), and the merge of Eq. lse-merge needs no explicit
-// backward: each ring-step block and the branch-local keys contribute
-//   dV += P^T dO,  dS = P o (dP - Delta) with dP = dO V^T and
-//   Delta = <dO, O>,  dK += scale dS^T Q,  dQ += scale dS K.
+// With the final LSE of every row the probabilities of any key subset are
+// P = exp(S - LSE), so the merge of Eq. lse-merge needs no explicit backward:
+// every ring-step block and the branch-local keys contribute
+//   dV += P^T dO,  dS = P o (dP - Delta),  dP = dO V^T,  Delta = <dO, O>,
+//   dK += scale dS^T Q,  dQ += scale dS K.
 //
 // Kernels
-//   preprocess : Delta and LSE * log2(e) per (token, head); clears dQ sums.
-//   main       : one workgroup per 128 keys of one ring-step block, one
-//                sequence and one KV head (32 keys per wavefront, dK and dV in
-//                registers).  It walks the query tokens that see those keys in
-//                64-row tiles (tokens x the G heads of the KV head); dQ
-//                contributions are summed over the 128 keys through LDS and
-//                added to an fp32 accumulator with global atomics.
-//   branch     : branch-local keys (at most 64 per group), vector ALUs.
-//   finalize   : dQ = scale * sums, converted to the output dtype.
+//   preprocess : Delta and LSE * log2(e) per (query token, head).
+//   kv         : dK and dV.  One workgroup per 128 keys of one ring-step
+//                block, sequence and KV head (32 keys per wavefront, dK/dV
+//                in registers); it walks the query tokens that reach those
+//                keys in 64-row tiles (tokens x the G heads of the KV head),
+//                double-buffered in LDS with register prefetch.  No atomics.
+//   dq         : dQ, query-tile parallel like the forward: per key tile
+//                S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T, with the
+//                branch-local keys handled in the epilogue.  Splitting dQ off
+//                costs two extra contractions but avoids fp32 atomics, whose
+//                throughput (about one 4-byte update per L2 channel and clock)
+//                would otherwise bound the whole backward.
+//   branch     : dK and dV of the branch-local keys (at most 64 per group).
 #include "ba_internal.h"
 #include "device_common.h"
 #include "kernels.h"
@@ -26,17 +30,7 @@ namespace ba {
 
 namespace {
 
-constexpr int kRowStride = kHeadDim + 8;  // padded row-major [rows][d] tiles
-constexpr int kKtStride = kBwdKeys + 8;   // K^T tile [d][keys]
-constexpr int kDsStride = kBwdKeys + 8;   // dS tile [rows][keys]
-
-// Transposed [d][64 rows] tile whose 16-byte chunk 2t+h holds rows
-// 16t+4h+{0..3} then 16t+8+4h+{0..3}, the rows a lane of half h feeds into
-// k-block t of an MFMA from an accumulator.  XOR-swizzled per d.
-__device__ __forceinline__ int tr_index(int d, int lchunk) {
-  const int sw = (d ^ (d >> 3)) & 7;
-  return d * kBwdRows + ((lchunk ^ sw) << 3);
-}
+constexpr int kRowStride = kHeadDim + 8;  // padded row-major [rows][d] LDS tiles
 
 __device__ __forceinline__ const bf16* row_ptr(const bf16* main, const bf16* br, int32_t qrow,
                                                int32_t hq, int32_t head) {
@@ -52,8 +46,8 @@ __device__ __forceinline__ void store_grad(void* base, int64_t idx, float v, boo
 }  // namespace
 
 // ------------------------------------------------------------ preprocess
-// 32 lanes per (token, head): Delta = <dO, O> over 128 dims, the row's LSE in
-// log2 units, and a cleared dQ accumulator row.
+// 32 lanes per (token, head): Delta = <dO, O> over 128 dims, and the row's
+// LSE in log2 units.
 __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
   const int64_t pair = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 5;
   const int sub = threadIdx.x & 31;
@@ -69,7 +63,6 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
               (float)ov[3] * (float)gv[3];
 #pragma unroll
   for (int m = 16; m >= 1; m >>= 1) dlt += __shfl_xor(dlt, m, 32);
-  reinterpret_cast<float4*>(p.dq_acc + pair * kHeadDim)[sub] = make_float4(0.f, 0.f, 0.f, 0.f);
   if (sub == 0) {
     const float lse = tk.qrow >= 0 ? p.lse_main[(int64_t)head * p.n_local + tk.qrow]
                                    : p.lse_br[(int64_t)head * p.n_br + (-tk.qrow - 1)];
@@ -77,17 +70,80 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
   }
 }
 
-// ------------------------------------------------------------ main (ring)
-__global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdParams p) {
-  __shared__ __attribute__((aligned(16))) bf16 q_s[kBwdRows * kRowStride];
-  __shared__ __attribute__((aligned(16))) bf16 do_s[kBwdRows * kRowStride];
-  __shared__ __attribute__((aligned(16))) bf16 qt_s[kHeadDim * kBwdRows];
-  __shared__ __attribute__((aligned(16))) bf16 dot_s[kHeadDim * kBwdRows];
-  __shared__ __attribute__((aligned(16))) bf16 ds_s[kBwdRows * kDsStride];
-  __shared__ __attribute__((aligned(16))) bf16 kt_s[kHeadDim * kKtStride];
-  __shared__ __attribute__((aligned(16))) float lse_s[kBwdRows];
-  __shared__ __attribute__((aligned(16))) float dlt_s[kBwdRows];
-  __shared__ __attribute__((aligned(16))) int lim_s[kBwdRows];
+// ------------------------------------------------------------ kv (ring)
+namespace {
+
+// Global loads of one 64-row query tile: this thread's 4 rows x 8 dims of Q
+// and dO, plus (threads 0..63) the row statistics and visible-key limit.
+struct QTileRegs {
+  bf16x8 q[4], g[4];
+  float l2, dl;
+  int lim;
+};
+
+__device__ __forceinline__ void load_qtile(const BwdParams& p, const BwdTile& tile, const SeqInfo& seq,
+                                           int qt0, int tid, QTileRegs& r) {
+  const int G = p.G;
+  const int tpt = kBwdRows / G;  // rows past tpt*G belong to no token
+  const int rg = tid >> 4, dc = tid & 15;  // rows 4rg..4rg+3, dims 8dc..8dc+7
+#pragma unroll
+  for (int r4 = 0; r4 < 4; ++r4) {
+    const int row = 4 * rg + r4;
+    const int tl = row / G;
+    const int tok = qt0 + tl;
+    if (tl < tpt && tok < tile.q_end) {
+      const TokInfo tk = p.toks[tok];
+      const int head = tile.kvh * G + (row - tl * G);
+      r.q[r4] = ld16(row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head) + 8 * dc);
+      r.g[r4] = ld16(row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head) + 8 * dc);
+    } else {
+      r.q[r4] = bf16x8{};
+      r.g[r4] = bf16x8{};
+    }
+  }
+  r.l2 = 0.f;
+  r.dl = 0.f;
+  r.lim = 0;
+  if (tid < kBwdRows) {
+    const int tl = tid / G;
+    const int tok = qt0 + tl;
+    if (tl < tpt && tok < tile.q_end) {
+      const int head = tile.kvh * G + (tid - tl * G);
+      const float2 rs = p.rowstat[(int64_t)tok * p.hq + head];
+      r.l2 = rs.x;
+      r.dl = rs.y;
+      int lim = visible_keys(p.toks[tok].P, tile.step, p.C, seq.c) - tile.u0;
+      r.lim = lim < tile.nk ? lim : tile.nk;
+    }
+  }
+}
+
+struct QTileLds {
+  bf16 q[kBwdRows * kRowStride];
+  bf16 g[kBwdRows * kRowStride];
+  float l2[kBwdRows];
+  float dl[kBwdRows];
+  int lim[kBwdRows];
+};
+
+__device__ __forceinline__ void store_qtile(QTileLds& s, const QTileRegs& r, int tid) {
+  const int rg = tid >> 4, dc = tid & 15;
+#pragma unroll
+  for (int r4 = 0; r4 < 4; ++r4) {
+    st16(&s.q[(4 * rg + r4) * kRowStride + 8 * dc], r.q[r4]);
+    st16(&s.g[(4 * rg + r4) * kRowStride + 8 * dc], r.g[r4]);
+  }
+  if (tid < kBwdRows) {
+    s.l2[tid] = r.l2;
+    s.dl[tid] = r.dl;
+    s.lim[tid] = r.lim;
+  }
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(256, 1) void bwd_kv_kernel(BwdParams p) {
+  __shared__ __attribute__((aligned(16))) QTileLds qs[2];
 
   const BwdTile tile = p.tiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
@@ -110,25 +166,6 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdParams p) {
     kreg[c] = ld16(kbase + (int64_t)kload * kv_row_stride + 16 * c + 8 * half);
     vreg[c] = ld16(vbase + (int64_t)kload * kv_row_stride + 16 * c + 8 * half);
   }
-  // K^T tile for dQ = dS K: kt_s[d][key]
-  {
-    const int kg = tid >> 3, dc = tid & 7;  // keys 4kg..4kg+3, dims 16dc..16dc+15
-    bf16x8 kv[4][2];
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      int u = 4 * kg + r4;
-      u = u < tile.nk ? u : tile.nk - 1;
-      kv[r4][0] = ld16(kbase + (int64_t)u * kv_row_stride + 16 * dc);
-      kv[r4][1] = ld16(kbase + (int64_t)u * kv_row_stride + 16 * dc + 8);
-    }
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      bf16x4 w;
-      w[0] = kv[0][e >> 3][e & 7]; w[1] = kv[1][e >> 3][e & 7];
-      w[2] = kv[2][e >> 3][e & 7]; w[3] = kv[3][e >> 3][e & 7];
-      *reinterpret_cast<bf16x4*>(&kt_s[(16 * dc + e) * kKtStride + 4 * kg]) = w;
-    }
-  }
 
   f32x16 dk[4], dv[4];
 #pragma unroll
@@ -137,64 +174,25 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdParams p) {
     dv[nt] = f32x16{};
   }
 
-  const int G = p.G;
-  const int tpt = kBwdRows / G;  // tokens per query tile
-  for (int qt0 = tile.q_begin; qt0 < tile.q_end; qt0 += tpt) {
-    __syncthreads();  // previous tile's LDS reads are done (and kt_s is written)
-    // ---- stage Q, dO (row-major and transposed) and the row statistics
-    {
-      const int rg = tid >> 4, dc = tid & 15;  // rows 4rg..4rg+3, dims 8dc..8dc+7
-      bf16x8 qv[4], gv[4];
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int r = 4 * rg + r4;
-        const int tl = r / G;
-        const int tok = qt0 + tl;
-        if (tok < tile.q_end) {
-          const TokInfo tk = p.toks[tok];
-          const int head = tile.kvh * G + (r - tl * G);
-          qv[r4] = ld16(row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head) + 8 * dc);
-          gv[r4] = ld16(row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head) + 8 * dc);
-        } else {
-          qv[r4] = bf16x8{};
-          gv[r4] = bf16x8{};
-        }
-        st16(&q_s[r * kRowStride + 8 * dc], qv[r4]);
-        st16(&do_s[r * kRowStride + 8 * dc], gv[r4]);
-      }
-      const int tb = rg >> 2, a = (rg & 3) >> 1, b = rg & 1;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int d = 8 * dc + e;
-        bf16x4 w;
-        w[0] = qv[0][e]; w[1] = qv[1][e]; w[2] = qv[2][e]; w[3] = qv[3][e];
-        *reinterpret_cast<bf16x4*>(&qt_s[tr_index(d, 2 * tb + b) + 4 * a]) = w;
-        w[0] = gv[0][e]; w[1] = gv[1][e]; w[2] = gv[2][e]; w[3] = gv[3][e];
-        *reinterpret_cast<bf16x4*>(&dot_s[tr_index(d, 2 * tb + b) + 4 * a]) = w;
-      }
-    }
-    if (tid < kBwdRows) {
-      const int r = tid;
-      const int tl = r / G;
-      const int tok = qt0 + tl;
-      float l2 = 0.f, dl = 0.f;
-      int lim = 0;
-      if (tok < tile.q_end) {
-        const int head = tile.kvh * G + (r - tl * G);
-        const float2 rs = p.rowstat[(int64_t)tok * p.hq + head];
-        l2 = rs.x;
-        dl = rs.y;
-        lim = visible_keys(p.toks[tok].P, tile.step, p.C, seq.c) - tile.u0;
-        lim = lim < tile.nk ? lim : tile.nk;
-      }
-      lse_s[r] = l2;
-      dlt_s[r] = dl;
-      lim_s[r] = lim;
-    }
-    __syncthreads();
-    const bool need_mask = qt0 < tile.q_full || qt0 + tpt > tile.q_end || tile.nk < kBwdKeys;
+  const int tpt = kBwdRows / p.G;  // tokens per query tile
+  const int ntiles = (tile.q_end - tile.q_begin + tpt - 1) / tpt;
+  {
+    QTileRegs r;
+    load_qtile(p, tile, seq, tile.q_begin, tid, r);
+    store_qtile(qs[0], r, tid);
+  }
+  __syncthreads();
 
-    // ---- S = Q K^T and dP = dO V^T (rows = queries, columns = this lane's key)
+  for (int it = 0; it < ntiles; ++it) {
+    const int qt0 = tile.q_begin + it * tpt;
+    const QTileLds& cur = qs[it & 1];
+    const bool more = it + 1 < ntiles;
+    QTileRegs nxt;
+    if (more) load_qtile(p, tile, seq, qt0 + tpt, tid, nxt);  // in flight during the MFMAs below
+    const bool need_mask =
+        qt0 < tile.q_full || qt0 + tpt > tile.q_end || tile.nk < kBwdKeys || tpt * p.G < kBwdRows;
+
+    // ---- S = Q K^T, dP = dO V^T (rows = queries, column = this lane's key)
     f32x16 s[2], dp[2];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
@@ -202,8 +200,8 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdParams p) {
       dp[mt] = f32x16{};
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
-        s[mt] = mfma32(ld16(&q_s[(32 * mt + qi) * kRowStride + 16 * c + 8 * half]), kreg[c], s[mt]);
-        dp[mt] = mfma32(ld16(&do_s[(32 * mt + qi) * kRowStride + 16 * c + 8 * half]), vreg[c], dp[mt]);
+        s[mt] = mfma32(ld16(&cur.q[(32 * mt + qi) * kRowStride + 16 * c + 8 * half]), kreg[c], s[mt]);
+        dp[mt] = mfma32(ld16(&cur.g[(32 * mt + qi) * kRowStride + 16 * c + 8 * half]), vreg[c], dp[mt]);
       }
     }
     // ---- P = exp2(S scale log2e - LSE log2e), dS = P (dP - Delta)
@@ -212,9 +210,9 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdParams p) {
 #pragma unroll
       for (int vq = 0; vq < 4; ++vq) {
         const int r0 = 32 * mt + 8 * vq + 4 * half;
-        const float4 l4 = *reinterpret_cast<const float4*>(&lse_s[r0]);
-        const float4 d4 = *reinterpret_cast<const float4*>(&dlt_s[r0]);
-        const int4 m4 = *reinterpret_cast<const int4*>(&lim_s[r0]);
+        const float4 l4 = *reinterpret_cast<const float4*>(&cur.l2[r0]);
+        const float4 d4 = *reinterpret_cast<const float4*>(&cur.dl[r0]);
+        const int4 m4 = *reinterpret_cast<const int4*>(&cur.lim[r0]);
         const float lr[4] = {l4.x, l4.y, l4.z, l4.w};
         const float dr[4] = {d4.x, d4.y, d4.z, d4.w};
         const int mr[4] = {m4.x, m4.y, m4.z, m4.w};
@@ -228,65 +226,30 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdParams p) {
         }
       }
     }
-    // ---- dV += P^T dO, dK += dS^T Q (k-block t = query rows 16t..16t+15)
-    bf16x8 pa[4], dsa[4];
+    // ---- dV += P^T dO, dK += dS^T Q.  k-block t covers query rows 16t..16t+15;
+    // a lane of half h holds rows 16t+4h+{0..3} and 16t+8+4h+{0..3} of it, so
+    // the dO / Q operand is read column-wise from the same rows.
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int v0 = 8 * (t & 1);
       const f32x16& ps = s[t >> 1];
       const f32x16& dss = dp[t >> 1];
-      pa[t] = pack8(ps[v0], ps[v0 + 1], ps[v0 + 2], ps[v0 + 3], ps[v0 + 4], ps[v0 + 5], ps[v0 + 6], ps[v0 + 7]);
-      dsa[t] = pack8(dss[v0], dss[v0 + 1], dss[v0 + 2], dss[v0 + 3], dss[v0 + 4], dss[v0 + 5], dss[v0 + 6],
-                     dss[v0 + 7]);
-    }
+      const bf16x8 pa = pack8(ps[v0], ps[v0 + 1], ps[v0 + 2], ps[v0 + 3], ps[v0 + 4], ps[v0 + 5], ps[v0 + 6],
+                              ps[v0 + 7]);
+      const bf16x8 dsa = pack8(dss[v0], dss[v0 + 1], dss[v0 + 2], dss[v0 + 3], dss[v0 + 4], dss[v0 + 5],
+                               dss[v0 + 6], dss[v0 + 7]);
+      const int ka = 16 * t + 4 * half, kb = 16 * t + 8 + 4 * half;
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        dv[nt] = mfma32(pa[t], ld16(&dot_s[tr_index(32 * nt + qi, 2 * t + half)]), dv[nt]);
-        dk[nt] = mfma32(dsa[t], ld16(&qt_s[tr_index(32 * nt + qi, 2 * t + half)]), dk[nt]);
+      for (int nt = 0; nt < 4; ++nt) {
+        dv[nt] = mfma32(pa, ld_tr8(cur.g, kRowStride, 32 * nt, ka, kb, lane), dv[nt]);
+        dk[nt] = mfma32(dsa, ld_tr8(cur.q, kRowStride, 32 * nt, ka, kb, lane), dk[nt]);
       }
     }
-    // ---- dS (bf16) to LDS as [row][key] for dQ = dS K
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = 32 * mt + 8 * (v >> 2) + 4 * half + (v & 3);
-        ds_s[r * kDsStride + my_key] = (bf16)dp[mt][v];
-      }
+    if (more) store_qtile(qs[(it + 1) & 1], nxt, tid);
     __syncthreads();
-    // ---- dQ tile (64 rows x 128 dims): wave w takes rows 32*(w&1).., dims 64*(w>>1)..
-    {
-      const int mt = wave & 1;
-      f32x16 dq[2];
-      dq[0] = f32x16{};
-      dq[1] = f32x16{};
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const bf16x8 a = ld16(&ds_s[(32 * mt + qi) * kDsStride + 16 * c + 8 * half]);
-#pragma unroll
-        for (int n = 0; n < 2; ++n) {
-          const int nt = 2 * (wave >> 1) + n;
-          dq[n] = mfma32(a, ld16(&kt_s[(32 * nt + qi) * kKtStride + 16 * c + 8 * half]), dq[n]);
-        }
-      }
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = 32 * mt + 8 * (v >> 2) + 4 * half + (v & 3);
-        const int tl = r / G;
-        const int tok = qt0 + tl;
-        if (tok < tile.q_end) {
-          const int head = tile.kvh * G + (r - tl * G);
-          float* dst = p.dq_acc + ((int64_t)tok * p.hq + head) * kHeadDim;
-#pragma unroll
-          for (int n = 0; n < 2; ++n) atomicAdd(dst + 32 * (2 * (wave >> 1) + n) + qi, dq[n][v]);
-        }
-      }
-    }
   }
 
-  // ---- write dK (scaled) and dV of this lane's... C layout: column = d, rows = keys
+  // ---- write dK (scaled) and dV: accumulator column = dim, rows = keys
   void* dkout = p.dk_step[tile.step];
   void* dvout = p.dv_step[tile.step];
 #pragma unroll
@@ -302,12 +265,218 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdParams p) {
     }
 }
 
-// ------------------------------------------------------------ branch-local
+// ------------------------------------------------------------ dq
+// Query tile of 128 rows (4 wavefronts x 32), the same tiles as the forward.
+// Accumulator layout: dQ^T, lane = one query row, rows = dims
+// 32*dt + 8*(v/4) + 4*half + v%4.
+template <int MODE>
+__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
+  __shared__ __attribute__((aligned(16))) bf16 ks[kFwdKeys * kRowStride];
+  __shared__ __attribute__((aligned(16))) bf16 vs[kFwdKeys * kRowStride];
+
+  const FwdTile tile = p.qtiles[blockIdx.x];
+  const SeqInfo seq = p.seqs[tile.seq];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int qi = lane & 31;
+  const int half = lane >> 5;
+  const int row = wave * 32 + qi;
+  const int tl = row / p.G;
+  const int head = tile.kvh * p.G + (row - tl * p.G);
+  const bool valid = tl < tile.ntok;
+  TokInfo tk;
+  if (valid) tk = p.toks[tile.tok_begin + tl];
+  else tk = TokInfo{0, -1, -1, -1};
+  const int64_t acc_row = (int64_t)(tile.tok_begin + tl) * p.hq + head;
+
+  bf16x8 qreg[8], greg[8];
+  float lse2 = 0.f, dlt = 0.f;
+  if (valid) {
+    const bf16* qp = row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head);
+    const bf16* gp = row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      qreg[c] = ld16(qp + 16 * c + 8 * half);
+      greg[c] = ld16(gp + 16 * c + 8 * half);
+    }
+    const float2 rs = p.rowstat[acc_row];
+    lse2 = rs.x;
+    dlt = rs.y;
+  } else {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      qreg[c] = bf16x8{};
+      greg[c] = bf16x8{};
+    }
+  }
+
+  f32x16 dq[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) dq[dt] = f32x16{};
+
+  const int Pmin = p.toks[tile.tok_begin].P;
+  const int Pmax = p.toks[tile.tok_begin + tile.ntok - 1].P;
+  const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
+
+  if (MODE != kModeFinal) {
+    for (int i = p.step_first; i < p.step_first + p.step_count; ++i) {
+      const int j = ((p.rank - i) % p.C + p.C) % p.C;
+      const int lim_lo = visible_keys(Pmin, j, p.C, seq.c);
+      const int lim_hi = visible_keys(Pmax, j, p.C, seq.c);
+      const int my_lim = valid ? visible_keys(tk.P, j, p.C, seq.c) : 0;
+      const bf16* kbase = p.k_step[j] + (int64_t)seq.seg_off * kv_row_stride + tile.kvh * kHeadDim;
+      const bf16* vbase = p.v_step[j] + (int64_t)seq.seg_off * kv_row_stride + tile.kvh * kHeadDim;
+      for (int kv0 = 0; kv0 < lim_hi; kv0 += kFwdKeys) {
+        {
+          const int kk = tid >> 2, qq = tid & 3;
+          int u = kv0 + kk;
+          u = u < lim_hi ? u : lim_hi - 1;
+          const bf16* ksrc = kbase + (int64_t)u * kv_row_stride + 32 * qq;
+          const bf16* vsrc = vbase + (int64_t)u * kv_row_stride + 32 * qq;
+#pragma unroll
+          for (int c8 = 0; c8 < 4; ++c8) {
+            st16(&ks[kk * kRowStride + 32 * qq + 8 * c8], ld16(ksrc + 8 * c8));
+            st16(&vs[kk * kRowStride + 32 * qq + 8 * c8], ld16(vsrc + 8 * c8));
+          }
+        }
+        __syncthreads();
+        // ---- S^T = K Q^T and dP^T = V dO^T (two 32-key sub-tiles)
+        f32x16 s[2], dp[2];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+          s[kt] = f32x16{};
+          dp[kt] = f32x16{};
+#pragma unroll
+          for (int c = 0; c < 8; ++c) {
+            s[kt] = mfma32(ld16(&ks[(32 * kt + qi) * kRowStride + 16 * c + 8 * half]), qreg[c], s[kt]);
+            dp[kt] = mfma32(ld16(&vs[(32 * kt + qi) * kRowStride + 16 * c + 8 * half]), greg[c], dp[kt]);
+          }
+        }
+        // ---- dS^T = P^T (dP^T - Delta), P^T = exp2(S^T scale log2e - LSE log2e)
+        const bool need_mask = kv0 + kFwdKeys > lim_lo;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            float pr = fast_exp2(s[kt][v] * p.scale_log2 - lse2);
+            if (need_mask) {
+              const int u = kv0 + 32 * kt + 8 * (v >> 2) + 4 * half + (v & 3);
+              pr = u < my_lim ? pr : 0.f;
+            }
+            dp[kt][v] = pr * (dp[kt][v] - dlt);
+          }
+        // ---- dQ^T += K^T dS^T: k-block t = keys 16t.. of the tile; the lane's
+        // dS^T values of half h are keys 16t+4h+{0..3}, 16t+8+4h+{0..3}
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const f32x16& src = dp[t >> 1];
+          const int v0 = 8 * (t & 1);
+          const bf16x8 b = pack8(src[v0], src[v0 + 1], src[v0 + 2], src[v0 + 3], src[v0 + 4], src[v0 + 5],
+                                 src[v0 + 6], src[v0 + 7]);
+          const int ka = 16 * t + 4 * half, kb = 16 * t + 8 + 4 * half;
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma32(ld_tr8(ks, kRowStride, 32 * dt, ka, kb, lane), b, dq[dt]);
+        }
+        __syncthreads();
+      }
+    }
+  }
+
+  if (MODE == kModeStep) {
+    if (!valid) return;
+    float* dst = p.dq_acc + acc_row * kHeadDim;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int vq = 0; vq < 4; ++vq) {
+        float4* d4 = reinterpret_cast<float4*>(dst + 32 * dt + 8 * vq + 4 * half);
+        float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (!p.acc_first) a = *d4;
+        a.x += dq[dt][4 * vq + 0];
+        a.y += dq[dt][4 * vq + 1];
+        a.z += dq[dt][4 * vq + 2];
+        a.w += dq[dt][4 * vq + 3];
+        *d4 = a;
+      }
+    return;
+  }
+  if (MODE == kModeFinal && valid) {
+    const float* src = p.dq_acc + acc_row * kHeadDim;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int vq = 0; vq < 4; ++vq) {
+        const float4 a = *reinterpret_cast<const float4*>(src + 32 * dt + 8 * vq + 4 * half);
+        dq[dt][4 * vq + 0] = a.x;
+        dq[dt][4 * vq + 1] = a.y;
+        dq[dt][4 * vq + 2] = a.z;
+        dq[dt][4 * vq + 3] = a.w;
+      }
+  }
+
+  // ---- branch-local keys of this row (vector ALUs)
+  int nb = 0;
+  GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
+  if (valid && tk.grp >= 0) {
+    gi = p.groups[tk.grp];
+    nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk.gidx + 1 : gi.len;
+  }
+  for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
+    const bool active = b < nb;
+    if (__ballot(active) == 0) break;
+    const int64_t krow = (int64_t)gi.row0 + (int64_t)b * gi.stride;
+    const bf16* kb = p.k_br + krow * kv_row_stride + tile.kvh * kHeadDim;
+    const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
+    float sdot = 0.f, pdot = 0.f;
+    if (active) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const bf16x8 kv = ld16(kb + 16 * c + 8 * half);
+        const bf16x8 vv = ld16(vb + 16 * c + 8 * half);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          sdot += (float)qreg[c][e] * (float)kv[e];
+          pdot += (float)greg[c][e] * (float)vv[e];
+        }
+      }
+    }
+    sdot += xor32(sdot);
+    pdot += xor32(pdot);
+    if (!active) continue;
+    const float pr = fast_exp2(sdot * p.scale_log2 - lse2);
+    const float ds = pr * (pdot - dlt);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int vq = 0; vq < 4; ++vq) {
+        const bf16x4 kk = *reinterpret_cast<const bf16x4*>(kb + 32 * dt + 8 * vq + 4 * half);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) dq[dt][4 * vq + c] += ds * (float)kk[c];
+      }
+  }
+  if (!valid) return;
+
+  void* out = tk.qrow >= 0 ? p.dq_main : p.dq_br;
+  const int64_t orow = tk.qrow >= 0 ? tk.qrow : -tk.qrow - 1;
+  const int64_t base = (orow * p.hq + head) * kHeadDim;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int vq = 0; vq < 4; ++vq) {
+      const int64_t o = base + 32 * dt + 8 * vq + 4 * half;
+      const float a0 = dq[dt][4 * vq] * p.scale, a1 = dq[dt][4 * vq + 1] * p.scale;
+      const float a2 = dq[dt][4 * vq + 2] * p.scale, a3 = dq[dt][4 * vq + 3] * p.scale;
+      if (p.grad_f32) *reinterpret_cast<float4*>(static_cast<float*>(out) + o) = make_float4(a0, a1, a2, a3);
+      else *reinterpret_cast<bf16x4*>(static_cast<bf16*>(out) + o) = pack4(a0, a1, a2, a3);
+    }
+}
+
+// ------------------------------------------------------------ branch dK/dV
 // One workgroup per (group, KV head).  Each wavefront takes query rows
-// (member i, head) in turn; lanes hold two dims each.  Scores and dP need a
-// wavefront-wide reduction per key.  dK/dV of the group's keys are summed in
-// LDS (fp32) and written once; a dQ row is owned by one wavefront and updated
-// in place (the ring kernel has finished with it).
+// (member i, head) in turn; lanes hold two dims each and every score needs a
+// wavefront-wide reduction.  The group's dK/dV are summed in LDS (fp32) and
+// written once.
 __global__ __launch_bounds__(256) void bwd_branch_kernel(BwdParams p) {
   extern __shared__ float acc_s[];  // [2][len][128]: dK sums, dV sums
   const int g = blockIdx.x / p.hkv;
@@ -325,42 +494,28 @@ __global__ __launch_bounds__(256) void bwd_branch_kernel(BwdParams p) {
     const int64_t brow = (int64_t)gi.row0 + (int64_t)i * gi.stride;
     const bf16* q = p.q_br + (brow * p.hq + head) * kHeadDim;
     const bf16* g_ = p.do_br + (brow * p.hq + head) * kHeadDim;
-    // row statistics: recomputed from O and the final LSE of this branch row
-    const bf16* o = p.o_br + (brow * p.hq + head) * kHeadDim;
+    const float2 rs = p.rowstat[(int64_t)(gi.tok0 + i) * p.hq + head];
     const float q0 = (float)q[2 * lane], q1 = (float)q[2 * lane + 1];
     const float g0 = (float)g_[2 * lane], g1 = (float)g_[2 * lane + 1];
-    float dlt = g0 * (float)o[2 * lane] + g1 * (float)o[2 * lane + 1];
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) dlt += __shfl_xor(dlt, m);
-    const float lse2 = p.lse_br[(int64_t)head * p.n_br + brow] * kLog2e;
     const int nk = gi.kind == BA_KIND_EAGLE_CHAIN ? i + 1 : n;
-    float dq0 = 0.f, dq1 = 0.f;
     for (int j = 0; j < nk; ++j) {
       const int64_t krow = (int64_t)gi.row0 + (int64_t)j * gi.stride;
       const bf16* kp = p.k_br + krow * kv_row_stride + kvh * kHeadDim;
       const bf16* vp = p.v_br + krow * kv_row_stride + kvh * kHeadDim;
-      const float k0 = (float)kp[2 * lane], k1 = (float)kp[2 * lane + 1];
-      const float v0 = (float)vp[2 * lane], v1 = (float)vp[2 * lane + 1];
-      float sdot = q0 * k0 + q1 * k1;
-      float pdot = g0 * v0 + g1 * v1;
+      float sdot = q0 * (float)kp[2 * lane] + q1 * (float)kp[2 * lane + 1];
+      float pdot = g0 * (float)vp[2 * lane] + g1 * (float)vp[2 * lane + 1];
 #pragma unroll
       for (int m = 32; m >= 1; m >>= 1) {
         sdot += __shfl_xor(sdot, m);
         pdot += __shfl_xor(pdot, m);
       }
-      const float pr = fast_exp2(sdot * p.scale_log2 - lse2);
-      const float ds = pr * (pdot - dlt);
-      dq0 += ds * k0;
-      dq1 += ds * k1;
+      const float pr = fast_exp2(sdot * p.scale_log2 - rs.x);
+      const float ds = pr * (pdot - rs.y);
       atomicAdd(&acc_s[j * kHeadDim + 2 * lane], ds * q0);
       atomicAdd(&acc_s[j * kHeadDim + 2 * lane + 1], ds * q1);
       atomicAdd(&acc_s[(n + j) * kHeadDim + 2 * lane], pr * g0);
       atomicAdd(&acc_s[(n + j) * kHeadDim + 2 * lane + 1], pr * g1);
     }
-    // group members are consecutive query tokens starting at gi.tok0
-    float* dq = p.dq_acc + ((int64_t)(gi.tok0 + i) * p.hq + head) * kHeadDim;
-    dq[2 * lane] += dq0;
-    dq[2 * lane + 1] += dq1;
   }
   __syncthreads();
   for (int idx = tid; idx < n * kHeadDim; idx += blockDim.x) {
@@ -369,29 +524,6 @@ __global__ __launch_bounds__(256) void bwd_branch_kernel(BwdParams p) {
     const int64_t o = krow * kv_row_stride + kvh * kHeadDim + d;
     store_grad(p.dk_br, o, acc_s[idx] * p.scale, p.grad_f32);
     store_grad(p.dv_br, o, acc_s[n * kHeadDim + idx], p.grad_f32);
-  }
-}
-
-// ------------------------------------------------------------ finalize
-// dQ = scale * (ring + branch-local sums), converted and scattered to the
-// caller's layout.  One thread per 4 dims of a (token, head) row.
-__global__ __launch_bounds__(256) void bwd_finalize_kernel(BwdParams p) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t pair = i >> 5;
-  const int sub = (int)(i & 31);
-  if (pair >= (int64_t)p.num_tokens * p.hq) return;
-  const int32_t t = (int32_t)(pair / p.hq);
-  const int32_t head = (int32_t)(pair - (int64_t)t * p.hq);
-  const TokInfo tk = p.toks[t];
-  float4 a = reinterpret_cast<const float4*>(p.dq_acc + pair * kHeadDim)[sub];
-  a.x *= p.scale; a.y *= p.scale; a.z *= p.scale; a.w *= p.scale;
-  void* out = tk.qrow >= 0 ? p.dq_main : p.dq_br;
-  const int64_t row = tk.qrow >= 0 ? tk.qrow : -tk.qrow - 1;
-  const int64_t base = (row * p.hq + head) * kHeadDim + 4 * sub;
-  if (p.grad_f32) {
-    *reinterpret_cast<float4*>(static_cast<float*>(out) + base) = a;
-  } else {
-    *reinterpret_cast<bf16x4*>(static_cast<bf16*>(out) + base) = pack4(a.x, a.y, a.z, a.w);
   }
 }
 
@@ -412,9 +544,18 @@ hipError_t launch_bwd_preprocess(const BwdParams& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_main(const BwdParams& p, hipStream_t stream) {
+hipError_t launch_bwd_kv(const BwdParams& p, hipStream_t stream) {
   if (p.num_tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(bwd_main_kernel, dim3(p.num_tiles), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL(bwd_kv_kernel, dim3(p.num_tiles), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq(const BwdParams& p, int mode, hipStream_t stream) {
+  if (p.num_qtiles == 0) return hipSuccess;
+  dim3 grid(p.num_qtiles), block(256);
+  if (mode == kModeStep) hipLaunchKernelGGL(bwd_dq_kernel<kModeStep>, grid, block, 0, stream, p);
+  else if (mode == kModeFinal) hipLaunchKernelGGL(bwd_dq_kernel<kModeFinal>, grid, block, 0, stream, p);
+  else hipLaunchKernelGGL(bwd_dq_kernel<kModeFused>, grid, block, 0, stream, p);
   return hipGetLastError();
 }
 
@@ -422,13 +563,6 @@ hipError_t launch_bwd_branch(const BwdParams& p, int max_group_len, hipStream_t 
   if (p.num_groups == 0) return hipSuccess;
   const size_t lds = (size_t)2 * max_group_len * kHeadDim * sizeof(float);
   hipLaunchKernelGGL(bwd_branch_kernel, dim3(p.num_groups * p.hkv), dim3(256), lds, stream, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_bwd_finalize(const BwdParams& p, hipStream_t stream) {
-  const int64_t threads = (int64_t)p.num_tokens * p.hq * 32;
-  if (threads == 0) return hipSuccess;
-  hipLaunchKernelGGL(bwd_finalize_kernel, dim3(grid_for(threads)), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 

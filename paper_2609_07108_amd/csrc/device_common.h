@@ -43,6 +43,28 @@ __device__ __forceinline__ bf16x4 pack4(float a0, float a1, float a2, float a3) 
 
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
 
+// ds_read_b64_tr_b16: inside every group of 16 lanes, lane i receives element
+// i%4 of the 8-byte chunks addressed by lanes 4e + i/4 (e = 0..3).  If lane j
+// addresses row k0 + j/4, column n0 + 4*(j%4) of a row-major tile T[k][n],
+// lane i therefore receives the column T[k0+e][n0+i], e = 0..3.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x4 ld_tr4(const bf16* p) {
+  const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+  return __builtin_bit_cast(bf16x4, r);
+}
+
+// MFMA operand (8 reduction values per lane) read column-wise from a
+// row-major LDS tile T (row stride `rs` elements): lane l takes column
+// n0 + l%32; its reduction slots 0..3 come from rows ka..ka+3 and slots 4..7
+// from rows kb..kb+3 (ka, kb may depend on the lane's half l/32).
+__device__ __forceinline__ bf16x8 ld_tr8(const bf16* T, int rs, int n0, int ka, int kb, int lane) {
+  const int i = lane & 15;
+  const int col = n0 + (lane & 16) + 4 * (i & 3);
+  const bf16x4 lo = ld_tr4(T + (ka + (i >> 2)) * rs + col);
+  const bf16x4 hi = ld_tr4(T + (kb + (i >> 2)) * rs + col);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 constexpr float kLog2e = 1.4426950408889634f;

@@ -42,8 +42,11 @@ struct BwdParams {
   const SeqInfo* seqs;
   const TokInfo* toks;
   const GroupInfo* groups;
-  const BwdTile* tiles;
+  const BwdTile* tiles;   // key tiles of the dK/dV kernel
   int32_t num_tiles;
+  const FwdTile* qtiles;  // query tiles of the dQ kernel
+  int32_t num_qtiles;
+  int32_t step_first, step_count, acc_first;
   int32_t C, rank, hq, hkv, G;
   int32_t num_tokens;
   int32_t num_groups;
@@ -71,14 +74,14 @@ struct BwdParams {
   void* dv_br;
   int32_t grad_f32;
   float2* rowstat;  // [T * hq]: (LSE * log2 e, Delta = <dO, O>)
-  float* dq_acc;    // [T * hq, d], unscaled dS K sums
+  float* dq_acc;    // [T * hq, d] running unscaled dS K sums (per-step schedule)
 };
 
 hipError_t launch_fwd(const FwdParams& p, int mode, hipStream_t stream);
 hipError_t launch_bwd_preprocess(const BwdParams& p, hipStream_t stream);
-hipError_t launch_bwd_main(const BwdParams& p, hipStream_t stream);
+hipError_t launch_bwd_kv(const BwdParams& p, hipStream_t stream);
+hipError_t launch_bwd_dq(const BwdParams& p, int mode, hipStream_t stream);
 hipError_t launch_bwd_branch(const BwdParams& p, int max_group_len, hipStream_t stream);
-hipError_t launch_bwd_finalize(const BwdParams& p, hipStream_t stream);
 hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t stream);
 
 }  // namespace ba

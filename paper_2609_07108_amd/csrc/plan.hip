@@ -57,8 +57,10 @@ WorkspaceLayout workspace_layout(const Plan& p, int mode) {
   off = after_tables;
   w.rowstat = off;
   off = align(off + rows * 2 * sizeof(float));
-  w.dq_acc = off;
-  off = align(off + rows * kHeadDim * sizeof(float));
+  if (mode == BA_MODE_PER_STEP) {
+    w.dq_acc = off;
+    off = align(off + rows * kHeadDim * sizeof(float));
+  }
   w.bwd_total = off;
   return w;
 }
@@ -133,7 +135,7 @@ static int build_plan(const ba_problem* pr, Plan& P) {
 
   // --- per sequence: token list ordered by causal limit
   P.seqs.resize(S);
-  double pairs = 0.0;
+  double pairs = 0.0, main_pairs = 0.0;
   int64_t local_off = 0;
   for (int32_t s = 0; s < S; ++s) {
     int32_t L = pr->cu_seqlens[s + 1] - pr->cu_seqlens[s];
@@ -163,6 +165,7 @@ static int build_plan(const ba_problem* pr, Plan& P) {
     });
     for (const TokInfo& t : tk) {
       pairs += (double)t.P + 1.0;
+      main_pairs += (double)t.P + 1.0;
       if (t.grp >= 0) {
         const ba_group& gr = pr->groups[t.grp];
         pairs += gr.kind == BA_KIND_EAGLE_CHAIN ? (double)(t.gidx + 1) : (double)gr.len;
@@ -175,6 +178,7 @@ static int build_plan(const ba_problem* pr, Plan& P) {
     local_off += 2 * c;
   }
   P.pairs_per_head = pairs;
+  P.main_pairs_per_head = main_pairs;
 
   // --- forward tiles: kFwdRows / G tokens x G heads, never across sequences
   const int32_t tpt = kFwdRows / G;
@@ -320,6 +324,13 @@ int branch_attn_useful_flops(const ba_plan* plan, double* fwd_flops, double* bwd
   double per = p.pairs_per_head * p.hq * p.head_dim;
   if (fwd_flops) *fwd_flops = 4.0 * per;
   if (bwd_flops) *bwd_flops = 10.0 * per;
+  return BA_OK;
+}
+
+int branch_attn_pair_counts(const ba_plan* plan, double* main_pairs, double* local_pairs) {
+  if (!plan) return ba::fail(BA_E_INVAL, "plan is NULL");
+  if (main_pairs) *main_pairs = plan->p.main_pairs_per_head;
+  if (local_pairs) *local_pairs = plan->p.pairs_per_head - plan->p.main_pairs_per_head;
   return BA_OK;
 }
 

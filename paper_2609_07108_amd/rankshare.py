@@ -43,27 +43,28 @@ class RankShare:
 
 
 def _layout_groups(prob: GlobalProblem, r: int, l2g: np.ndarray, layout: str):
-    C = prob.cp_size
     n_local = len(l2g)
-    glob_to_local = {int(g): i for i, g in enumerate(l2g)}
-    sel = []
-    for g in range(len(prob.g_seq)):
-        s = int(prob.g_seq[g])
-        gpos = int(prob.cu_seqlens[s]) + int(prob.g_anchor[g])
-        if gpos in glob_to_local:  # the anchor's main token lives on this rank
-            sel.append(g)
-    sel = np.asarray(sel, np.int64)
+    # a group belongs to this rank iff its anchor's main token is one of the rank's tokens
+    g_pos = prob.cu_seqlens[prob.g_seq] + prob.g_anchor if len(prob.g_seq) else np.zeros(0, np.int64)
+    order = np.argsort(l2g, kind="stable")
+    sorted_l2g = np.asarray(l2g, np.int64)[order]
+    idx = np.searchsorted(sorted_l2g, g_pos)
+    hit = (idx < len(sorted_l2g)) & (sorted_l2g[np.minimum(idx, len(sorted_l2g) - 1)] == g_pos) \
+        if len(sorted_l2g) else np.zeros(len(g_pos), bool)
+    sel = np.flatnonzero(hit).astype(np.int64)
+    anchor_local = order[idx[hit]] if len(sel) else np.zeros(0, np.int64)
     desc, loc_rows, glob_rows = [], [], []
     if layout == "group":
-        row = 0
-        for g in sel:
-            n = int(prob.g_len[g])
-            desc.append((int(prob.g_seq[g]), int(prob.g_anchor[g]), int(prob.g_kind[g]), n, row, 1))
-            loc_rows.append(np.arange(row, row + n))
-            glob_rows.append(np.arange(prob.g_row0[g], prob.g_row0[g] + n))
-            row += n
-        nrows = row
-    elif layout == "depth":
+        lens = prob.g_len[sel]
+        row0 = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64) if len(sel) else lens
+        desc = np.stack([prob.g_seq[sel], prob.g_anchor[sel], prob.g_kind[sel], lens, row0,
+                         np.ones(len(sel), np.int64)], axis=1) if len(sel) else np.zeros((0, 6))
+        member = np.arange(int(lens.sum())) - np.repeat(row0, lens) if len(sel) else np.zeros(0, np.int64)
+        loc = np.arange(int(lens.sum()), dtype=np.int64)
+        glob = np.repeat(prob.g_row0[sel], lens) + member if len(sel) else loc
+        return (np.asarray(desc, np.int32).reshape(-1, 6), sel, loc, glob.astype(np.int64), int(lens.sum()))
+    glob_to_local = {int(g): int(u) for g, u in zip(g_pos[sel], anchor_local)}
+    if layout == "depth":
         eag = [g for g in sel if prob.g_kind[g] == KIND_EAGLE]
         kmax = max([int(prob.g_len[g]) for g in eag], default=0)
         row = kmax * n_local
@@ -155,16 +156,17 @@ def workspace(share: RankShare, mode: int, backward: bool = False):
     return torch.empty(n, dtype=torch.uint8, device=share.t["q_main"].device)
 
 
-def run_fwd(share: RankShare, out: dict, mode: int, ws):
+def run_fwd(share: RankShare, out: dict, mode: int, ws, ring_events=(None, None)):
     t = share.t
     B.branch_attn_fwd(share.plan, mode, t["q_main"], t["q_br"], t["k_br"], t["v_br"], t["k_step"],
-                      t["v_step"], out["o_main"], out["o_br"], out["lse_main"], out["lse_br"], ws)
+                      t["v_step"], out["o_main"], out["o_br"], out["lse_main"], out["lse_br"], ws,
+                      ring_events=ring_events)
 
 
-def run_bwd(share: RankShare, out: dict, mode: int, ws):
+def run_bwd(share: RankShare, out: dict, mode: int, ws, ring_events=(None, None)):
     t = share.t
     gd = B.BA_DTYPE_F32 if out["dq_main"].dtype == torch.float32 else B.BA_DTYPE_BF16
     B.branch_attn_bwd(share.plan, mode, t["q_main"], t["q_br"], t["k_br"], t["v_br"], t["k_step"],
                       t["v_step"], out["o_main"], out["o_br"], out["lse_main"], out["lse_br"],
                       t["do_main"], t["do_br"], out["dq_main"], out["dq_br"], out["dk_step"],
-                      out["dv_step"], out["dk_br"], out["dv_br"], gd, ws)
+                      out["dv_step"], out["dk_br"], out["dv_br"], gd, ws, ring_events=ring_events)

@@ -35,6 +35,8 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -115,7 +117,9 @@ class GlobalProblem:
         sb = blocks[order]
         starts = np.flatnonzero(np.r_[True, sb[1:] != sb[:-1]])
         ends = np.r_[starts[1:], len(sb)]
-        for st, en in zip(starts, ends):
+
+        def one(se):
+            st, en = se
             b = int(sb[st])
             nrows = min(ROW_BLOCK, total - b * ROW_BLOCK)
             blk = np.random.default_rng([self.seed, tid, b]).standard_normal(
@@ -123,6 +127,15 @@ class GlobalProblem:
             blk_t = torch.from_numpy(blk).to(torch.bfloat16)
             sel = order[st:en]
             out[torch.from_numpy(sel)] = blk_t[torch.from_numpy(rows[sel] - b * ROW_BLOCK)]
+
+        jobs = list(zip(starts, ends))
+        if len(jobs) > 4:
+            # block streams are independent, so the draw order does not matter
+            with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+                list(ex.map(one, jobs))
+        else:
+            for j in jobs:
+                one(j)
         return out
 
 

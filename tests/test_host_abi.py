@@ -136,4 +136,6 @@ def test_workspace_sizes():
     n_local, ntok = share.plan.info()
     assert f_step >= ntok * prob.hq * 128 * 4  # running fp32 output
     assert f_fused < f_step
-    assert b_step == b_fused >= ntok * prob.hq * 128 * 4
+    # per-step backward keeps running fp32 dQ sums; the fused one needs only row statistics
+    assert b_step >= ntok * prob.hq * (128 + 2) * 4
+    assert ntok * prob.hq * 2 * 4 <= b_fused < b_step
