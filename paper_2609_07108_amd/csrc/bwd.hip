@@ -11,10 +11,10 @@
 // Kernels
 //   preprocess : Delta and LSE * log2(e) per (query token, head).
 //   kv         : dK and dV.  One workgroup per 128 keys of one ring-step
-//                block, sequence and KV head (32 keys per wavefront, dK/dV
-//                in registers); it walks the query tokens that reach those
-//                keys in 64-row tiles (tokens x the G heads of the KV head),
-//                double-buffered in LDS with register prefetch.  No atomics.
+//                block, sequence and KV head (dK/dV in registers); it walks
+//                the query tokens that reach those keys in 64-row tiles
+//                (tokens x the G heads of the KV head), double-buffered in
+//                LDS with register prefetch.  No atomics.
 //   dq         : dQ, query-tile parallel like the forward: per key tile
 //                S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T, with the
 //                branch-local keys handled in the epilogue.  Splitting dQ off
@@ -71,12 +71,39 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------ kv (ring)
+// Workgroup of 8 wavefronts (2 per SIMD) on 128 keys: wavefront w owns keys
+// 32*(w%4).. and the query rows 32*(w/4).. of every 64-row tile, so each key
+// group is covered by two wavefronts whose dK/dV partial sums are added
+// through LDS at the end.  The K and V tiles stay in LDS for the whole walk
+// (B operands of S = Q K^T and dP = dO V^T); the query tiles are
+// double-buffered in LDS and prefetched through registers.
 namespace {
 
-// Global loads of one 64-row query tile: this thread's 4 rows x 8 dims of Q
-// and dO, plus (threads 0..63) the row statistics and visible-key limit.
+constexpr int kKvWaves = 8;
+constexpr int kKvThreads = 64 * kKvWaves;
+
+struct QTileLds {
+  bf16 q[kBwdRows * kRowStride];
+  bf16 g[kBwdRows * kRowStride];
+  float l2[kBwdRows];
+  float dl[kBwdRows];
+  int lim[kBwdRows];
+};
+
+struct KvLds {
+  union {
+    QTileLds qs[2];
+    float red[4 * 64 * 64];  // end-of-kernel exchange of one accumulator set
+  };
+  bf16 k[kBwdKeys * kRowStride];
+  bf16 v[kBwdKeys * kRowStride];
+};
+
+// One thread's share of the next query tile: threads 0..255 load 4 rows x 8
+// dims of Q, threads 256..511 the same of dO; threads 0..63 also load the row
+// statistics and the visible-key limit.
 struct QTileRegs {
-  bf16x8 q[4], g[4];
+  bf16x8 x[4];
   float l2, dl;
   int lim;
 };
@@ -85,7 +112,9 @@ __device__ __forceinline__ void load_qtile(const BwdParams& p, const BwdTile& ti
                                            int qt0, int tid, QTileRegs& r) {
   const int G = p.G;
   const int tpt = kBwdRows / G;  // rows past tpt*G belong to no token
-  const int rg = tid >> 4, dc = tid & 15;  // rows 4rg..4rg+3, dims 8dc..8dc+7
+  const int t = tid & 255;
+  const bool is_do = tid >= 256;
+  const int rg = t >> 4, dc = t & 15;  // rows 4rg..4rg+3, dims 8dc..8dc+7
 #pragma unroll
   for (int r4 = 0; r4 < 4; ++r4) {
     const int row = 4 * rg + r4;
@@ -94,11 +123,10 @@ __device__ __forceinline__ void load_qtile(const BwdParams& p, const BwdTile& ti
     if (tl < tpt && tok < tile.q_end) {
       const TokInfo tk = p.toks[tok];
       const int head = tile.kvh * G + (row - tl * G);
-      r.q[r4] = ld16(row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head) + 8 * dc);
-      r.g[r4] = ld16(row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head) + 8 * dc);
+      r.x[r4] = ld16(row_ptr(is_do ? p.do_main : p.q_main, is_do ? p.do_br : p.q_br, tk.qrow, p.hq, head) +
+                     8 * dc);
     } else {
-      r.q[r4] = bf16x8{};
-      r.g[r4] = bf16x8{};
+      r.x[r4] = bf16x8{};
     }
   }
   r.l2 = 0.f;
@@ -118,21 +146,12 @@ __device__ __forceinline__ void load_qtile(const BwdParams& p, const BwdTile& ti
   }
 }
 
-struct QTileLds {
-  bf16 q[kBwdRows * kRowStride];
-  bf16 g[kBwdRows * kRowStride];
-  float l2[kBwdRows];
-  float dl[kBwdRows];
-  int lim[kBwdRows];
-};
-
 __device__ __forceinline__ void store_qtile(QTileLds& s, const QTileRegs& r, int tid) {
-  const int rg = tid >> 4, dc = tid & 15;
+  const int t = tid & 255;
+  const int rg = t >> 4, dc = t & 15;
+  bf16* dst = tid >= 256 ? s.g : s.q;
 #pragma unroll
-  for (int r4 = 0; r4 < 4; ++r4) {
-    st16(&s.q[(4 * rg + r4) * kRowStride + 8 * dc], r.q[r4]);
-    st16(&s.g[(4 * rg + r4) * kRowStride + 8 * dc], r.g[r4]);
-  }
+  for (int r4 = 0; r4 < 4; ++r4) st16(&dst[(4 * rg + r4) * kRowStride + 8 * dc], r.x[r4]);
   if (tid < kBwdRows) {
     s.l2[tid] = r.l2;
     s.dl[tid] = r.dl;
@@ -142,14 +161,16 @@ __device__ __forceinline__ void store_qtile(QTileLds& s, const QTileRegs& r, int
 
 }  // namespace
 
-__global__ __launch_bounds__(256, 1) void bwd_kv_kernel(BwdParams p) {
-  __shared__ __attribute__((aligned(16))) QTileLds qs[2];
+__global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
+  __shared__ __attribute__((aligned(16))) KvLds sm;
 
   const BwdTile tile = p.tiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  const int kw = wave & 3;   // key group
+  const int rh = wave >> 2;  // row half of every query tile
   const int qi = lane & 31;
   const int half = lane >> 5;
   const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
@@ -157,14 +178,18 @@ __global__ __launch_bounds__(256, 1) void bwd_kv_kernel(BwdParams p) {
   const bf16* kbase = p.k_step[tile.step] + key0 * kv_row_stride + tile.kvh * kHeadDim;
   const bf16* vbase = p.v_step[tile.step] + key0 * kv_row_stride + tile.kvh * kHeadDim;
 
-  // this lane's key (B operand of S = Q K^T and dP = dO V^T): key 32*wave+qi
-  const int my_key = 32 * wave + qi;
-  const int kload = my_key < tile.nk ? my_key : tile.nk - 1;
-  bf16x8 kreg[8], vreg[8];
+  // this lane's key (column of S and dP): key 32*kw+qi of the tile
+  const int my_key = 32 * kw + qi;
+  {
+    const int kk = tid >> 2, qq = tid & 3;  // K and V tiles: key kk, dims 32qq..32qq+31
+    const int u = kk < tile.nk ? kk : tile.nk - 1;
+    const bf16* ksrc = kbase + (int64_t)u * kv_row_stride + 32 * qq;
+    const bf16* vsrc = vbase + (int64_t)u * kv_row_stride + 32 * qq;
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    kreg[c] = ld16(kbase + (int64_t)kload * kv_row_stride + 16 * c + 8 * half);
-    vreg[c] = ld16(vbase + (int64_t)kload * kv_row_stride + 16 * c + 8 * half);
+    for (int c8 = 0; c8 < 4; ++c8) {
+      st16(&sm.k[kk * kRowStride + 32 * qq + 8 * c8], ld16(ksrc + 8 * c8));
+      st16(&sm.v[kk * kRowStride + 32 * qq + 8 * c8], ld16(vsrc + 8 * c8));
+    }
   }
 
   f32x16 dk[4], dv[4];
@@ -179,75 +204,97 @@ __global__ __launch_bounds__(256, 1) void bwd_kv_kernel(BwdParams p) {
   {
     QTileRegs r;
     load_qtile(p, tile, seq, tile.q_begin, tid, r);
-    store_qtile(qs[0], r, tid);
+    store_qtile(sm.qs[0], r, tid);
   }
   __syncthreads();
 
+  const int r0w = 32 * rh;  // first query row of this wavefront inside a tile
   for (int it = 0; it < ntiles; ++it) {
     const int qt0 = tile.q_begin + it * tpt;
-    const QTileLds& cur = qs[it & 1];
+    const QTileLds& cur = sm.qs[it & 1];
     const bool more = it + 1 < ntiles;
     QTileRegs nxt;
     if (more) load_qtile(p, tile, seq, qt0 + tpt, tid, nxt);  // in flight during the MFMAs below
     const bool need_mask =
         qt0 < tile.q_full || qt0 + tpt > tile.q_end || tile.nk < kBwdKeys || tpt * p.G < kBwdRows;
 
-    // ---- S = Q K^T, dP = dO V^T (rows = queries, column = this lane's key)
-    f32x16 s[2], dp[2];
+    // ---- S = Q K^T, dP = dO V^T (rows = this wavefront's 32 queries, column = the lane's key)
+    f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-      s[mt] = f32x16{};
-      dp[mt] = f32x16{};
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        s[mt] = mfma32(ld16(&cur.q[(32 * mt + qi) * kRowStride + 16 * c + 8 * half]), kreg[c], s[mt]);
-        dp[mt] = mfma32(ld16(&cur.g[(32 * mt + qi) * kRowStride + 16 * c + 8 * half]), vreg[c], dp[mt]);
-      }
+    for (int c = 0; c < 8; ++c) {
+      s = mfma32(ld16(&cur.q[(r0w + qi) * kRowStride + 16 * c + 8 * half]),
+                 ld16(&sm.k[my_key * kRowStride + 16 * c + 8 * half]), s);
+      dp = mfma32(ld16(&cur.g[(r0w + qi) * kRowStride + 16 * c + 8 * half]),
+                  ld16(&sm.v[my_key * kRowStride + 16 * c + 8 * half]), dp);
     }
     // ---- P = exp2(S scale log2e - LSE log2e), dS = P (dP - Delta)
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
+    for (int vq = 0; vq < 4; ++vq) {
+      const int r0 = r0w + 8 * vq + 4 * half;
+      const float4 l4 = *reinterpret_cast<const float4*>(&cur.l2[r0]);
+      const float4 d4 = *reinterpret_cast<const float4*>(&cur.dl[r0]);
+      const int4 m4 = *reinterpret_cast<const int4*>(&cur.lim[r0]);
+      const float lr[4] = {l4.x, l4.y, l4.z, l4.w};
+      const float dr[4] = {d4.x, d4.y, d4.z, d4.w};
+      const int mr[4] = {m4.x, m4.y, m4.z, m4.w};
 #pragma unroll
-      for (int vq = 0; vq < 4; ++vq) {
-        const int r0 = 32 * mt + 8 * vq + 4 * half;
-        const float4 l4 = *reinterpret_cast<const float4*>(&cur.l2[r0]);
-        const float4 d4 = *reinterpret_cast<const float4*>(&cur.dl[r0]);
-        const int4 m4 = *reinterpret_cast<const int4*>(&cur.lim[r0]);
-        const float lr[4] = {l4.x, l4.y, l4.z, l4.w};
-        const float dr[4] = {d4.x, d4.y, d4.z, d4.w};
-        const int mr[4] = {m4.x, m4.y, m4.z, m4.w};
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const int v = 4 * vq + c;
-          float pr = fast_exp2(s[mt][v] * p.scale_log2 - lr[c]);
-          if (need_mask && my_key >= mr[c]) pr = 0.f;
-          s[mt][v] = pr;
-          dp[mt][v] = pr * (dp[mt][v] - dr[c]);
-        }
+      for (int c = 0; c < 4; ++c) {
+        const int v = 4 * vq + c;
+        float pr = fast_exp2(s[v] * p.scale_log2 - lr[c]);
+        if (need_mask && my_key >= mr[c]) pr = 0.f;
+        s[v] = pr;
+        dp[v] = pr * (dp[v] - dr[c]);
       }
     }
-    // ---- dV += P^T dO, dK += dS^T Q.  k-block t covers query rows 16t..16t+15;
-    // a lane of half h holds rows 16t+4h+{0..3} and 16t+8+4h+{0..3} of it, so
+    // ---- dV += P^T dO, dK += dS^T Q.  k-block t covers rows r0w+16t..+15; a
+    // lane of half h holds rows 16t+4h+{0..3} and 16t+8+4h+{0..3} of it, so
     // the dO / Q operand is read column-wise from the same rows.
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int v0 = 8 * (t & 1);
-      const f32x16& ps = s[t >> 1];
-      const f32x16& dss = dp[t >> 1];
-      const bf16x8 pa = pack8(ps[v0], ps[v0 + 1], ps[v0 + 2], ps[v0 + 3], ps[v0 + 4], ps[v0 + 5], ps[v0 + 6],
-                              ps[v0 + 7]);
-      const bf16x8 dsa = pack8(dss[v0], dss[v0 + 1], dss[v0 + 2], dss[v0 + 3], dss[v0 + 4], dss[v0 + 5],
-                               dss[v0 + 6], dss[v0 + 7]);
-      const int ka = 16 * t + 4 * half, kb = 16 * t + 8 + 4 * half;
+    for (int t = 0; t < 2; ++t) {
+      const int v0 = 8 * t;
+      const bf16x8 pa = pack8(s[v0], s[v0 + 1], s[v0 + 2], s[v0 + 3], s[v0 + 4], s[v0 + 5], s[v0 + 6], s[v0 + 7]);
+      const bf16x8 dsa =
+          pack8(dp[v0], dp[v0 + 1], dp[v0 + 2], dp[v0 + 3], dp[v0 + 4], dp[v0 + 5], dp[v0 + 6], dp[v0 + 7]);
+      const int ka = r0w + 16 * t + 4 * half, kb = ka + 8;
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
         dv[nt] = mfma32(pa, ld_tr8(cur.g, kRowStride, 32 * nt, ka, kb, lane), dv[nt]);
         dk[nt] = mfma32(dsa, ld_tr8(cur.q, kRowStride, 32 * nt, ka, kb, lane), dk[nt]);
       }
     }
-    if (more) store_qtile(qs[(it + 1) & 1], nxt, tid);
+    if (more) store_qtile(sm.qs[(it + 1) & 1], nxt, tid);
     __syncthreads();
   }
+
+  // ---- add the two row halves' partial sums (wavefronts w and w+4), one
+  // accumulator set at a time through the (now idle) query-tile buffers
+  float* red = sm.red + (kw * 64) * 64;
+  if (rh == 1) {
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) red[(16 * nt + v) * 64 + lane] = dk[nt][v];
+  }
+  __syncthreads();
+  if (rh == 0) {
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) dk[nt][v] += red[(16 * nt + v) * 64 + lane];
+  }
+  __syncthreads();
+  if (rh == 1) {
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) red[(16 * nt + v) * 64 + lane] = dv[nt][v];
+  }
+  __syncthreads();
+  if (rh == 1) return;
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dv[nt][v] += red[(16 * nt + v) * 64 + lane];
 
   // ---- write dK (scaled) and dV: accumulator column = dim, rows = keys
   void* dkout = p.dk_step[tile.step];
@@ -256,7 +303,7 @@ __global__ __launch_bounds__(256, 1) void bwd_kv_kernel(BwdParams p) {
   for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int key = 32 * wave + 8 * (v >> 2) + 4 * half + (v & 3);
+      const int key = 32 * kw + 8 * (v >> 2) + 4 * half + (v & 3);
       if (key < tile.nk) {
         const int64_t idx = (key0 + key) * kv_row_stride + tile.kvh * kHeadDim + 32 * nt + qi;
         store_grad(dkout, idx, dk[nt][v] * p.scale, p.grad_f32);
@@ -546,7 +593,7 @@ hipError_t launch_bwd_preprocess(const BwdParams& p, hipStream_t stream) {
 
 hipError_t launch_bwd_kv(const BwdParams& p, hipStream_t stream) {
   if (p.num_tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(bwd_kv_kernel, dim3(p.num_tiles), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL(bwd_kv_kernel, dim3(p.num_tiles), dim3(kKvThreads), 0, stream, p);
   return hipGetLastError();
 }
 
