@@ -14,7 +14,7 @@
 //                block, sequence and KV head (dK/dV in registers); it walks
 //                the query tokens that reach those keys in 64-row tiles
 //                (tokens x the G heads of the KV head), double-buffered in
-//                LDS with register prefetch.  No atomics.
+//                LDS by direct global-to-LDS loads.  No atomics.
 //   dq         : dQ, query-tile parallel like the forward: per key tile
 //                S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T, with the
 //                branch-local keys handled in the epilogue.  Splitting dQ off
@@ -22,6 +22,8 @@
 //                throughput (about one 4-byte update per L2 channel and clock)
 //                would otherwise bound the whole backward.
 //   branch     : dK and dV of the branch-local keys (at most 64 per group).
+#include <type_traits>
+
 #include "ba_internal.h"
 #include "device_common.h"
 #include "kernels.h"
@@ -29,8 +31,6 @@
 namespace ba {
 
 namespace {
-
-constexpr int kRowStride = kHeadDim + 8;  // padded row-major [rows][d] LDS tiles
 
 __device__ __forceinline__ const bf16* row_ptr(const bf16* main, const bf16* br, int32_t qrow,
                                                int32_t hq, int32_t head) {
@@ -71,67 +71,58 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------ kv (ring)
-// Workgroup of 8 wavefronts (2 per SIMD) on 128 keys: wavefront w owns keys
-// 32*(w%4).. and the query rows 32*(w/4).. of every 64-row tile, so each key
-// group is covered by two wavefronts whose dK/dV partial sums are added
-// through LDS at the end.  The K and V tiles stay in LDS for the whole walk
-// (B operands of S = Q K^T and dP = dO V^T); the query tiles are
-// double-buffered in LDS and prefetched through registers.
+// Workgroup of 4 wavefronts (one per SIMD, so up to 512 registers each) on
+// 128 keys: wavefront w owns keys 32w..32w+31 against every 64-row query
+// tile.  K and V of its keys stay in registers (B operands of S = Q K^T and
+// dP = dO V^T), dK and dV accumulate in registers.  Query tiles (Q and dO)
+// are double-buffered plane tiles (see tile_off) fetched with direct
+// global-to-LDS loads while the previous one is in use; the loop is unrolled
+// by two so that each half works on a fixed buffer.
 namespace {
 
-constexpr int kKvWaves = 8;
+constexpr int kKvWaves = 4;
 constexpr int kKvThreads = 64 * kKvWaves;
 
 struct QTileLds {
-  bf16 q[kBwdRows * kRowStride];
-  bf16 g[kBwdRows * kRowStride];
+  bf16 q[kBwdRows * kHeadDim];
+  bf16 g[kBwdRows * kHeadDim];
   float l2[kBwdRows];
   float dl[kBwdRows];
   int lim[kBwdRows];
 };
 
-struct KvLds {
-  union {
-    QTileLds qs[2];
-    float red[4 * 64 * 64];  // end-of-kernel exchange of one accumulator set
-  };
-  bf16 k[kBwdKeys * kRowStride];
-  bf16 v[kBwdKeys * kRowStride];
-};
-
-// One thread's share of the next query tile: threads 0..255 load 4 rows x 8
-// dims of Q, threads 256..511 the same of dO; threads 0..63 also load the row
-// statistics and the visible-key limit.
-struct QTileRegs {
-  bf16x8 x[4];
+struct RowStats {
   float l2, dl;
   int lim;
 };
 
-__device__ __forceinline__ void load_qtile(const BwdParams& p, const BwdTile& tile, const SeqInfo& seq,
-                                           int qt0, int tid, QTileRegs& r) {
+// Issue the direct loads of the query tile starting at token qt0 into `s`:
+// wavefronts 0-1 fetch Q, 2-3 dO, eight loads of 16 rows x 32 columns each.
+// Rows without a token (past the range, or past tpt*G) fetch the tile's
+// first row: their probabilities are masked to zero, so only finiteness
+// matters.  Threads 0..63 also return the row statistics, written to LDS
+// once the buffer is no longer read.
+__device__ __forceinline__ RowStats fetch_qtile(const BwdParams& p, const BwdTile& tile, const SeqInfo& seq,
+                                               int qt0, int tid, QTileLds& s) {
   const int G = p.G;
-  const int tpt = kBwdRows / G;  // rows past tpt*G belong to no token
-  const int t = tid & 255;
-  const bool is_do = tid >= 256;
-  const int rg = t >> 4, dc = t & 15;  // rows 4rg..4rg+3, dims 8dc..8dc+7
+  const int tpt = kBwdRows / G;
+  const int lane = tid & 63, wave = tid >> 6;
+  const bool is_do = wave >= 2;
+  const bf16* mainp = is_do ? p.do_main : p.q_main;
+  const bf16* brp = is_do ? p.do_br : p.q_br;
+  bf16* dst = is_do ? s.g : s.q;
 #pragma unroll
-  for (int r4 = 0; r4 < 4; ++r4) {
-    const int row = 4 * rg + r4;
+  for (int m8 = 0; m8 < 8; ++m8) {
+    const int m = 8 * (wave & 1) + m8;
+    const int row = dma_row<kBwdRows>(m, lane);
     const int tl = row / G;
     const int tok = qt0 + tl;
-    if (tl < tpt && tok < tile.q_end) {
-      const TokInfo tk = p.toks[tok];
-      const int head = tile.kvh * G + (row - tl * G);
-      r.x[r4] = ld16(row_ptr(is_do ? p.do_main : p.q_main, is_do ? p.do_br : p.q_br, tk.qrow, p.hq, head) +
-                     8 * dc);
-    } else {
-      r.x[r4] = bf16x8{};
-    }
+    const bool ok = tl < tpt && tok < tile.q_end;
+    const TokInfo tk = p.toks[ok ? tok : qt0];
+    const int head = tile.kvh * G + (ok ? row - tl * G : 0);
+    dma16(row_ptr(mainp, brp, tk.qrow, p.hq, head) + dma_col<kBwdRows>(m, lane), dma_dst<kBwdRows>(dst, m));
   }
-  r.l2 = 0.f;
-  r.dl = 0.f;
-  r.lim = 0;
+  RowStats r{0.f, 0.f, 0};
   if (tid < kBwdRows) {
     const int tl = tid / G;
     const int tok = qt0 + tl;
@@ -140,18 +131,14 @@ __device__ __forceinline__ void load_qtile(const BwdParams& p, const BwdTile& ti
       const float2 rs = p.rowstat[(int64_t)tok * p.hq + head];
       r.l2 = rs.x;
       r.dl = rs.y;
-      int lim = visible_keys(p.toks[tok].P, tile.step, p.C, seq.c) - tile.u0;
+      const int lim = visible_keys(p.toks[tok].P, tile.step, p.C, seq.c) - tile.u0;
       r.lim = lim < tile.nk ? lim : tile.nk;
     }
   }
+  return r;
 }
 
-__device__ __forceinline__ void store_qtile(QTileLds& s, const QTileRegs& r, int tid) {
-  const int t = tid & 255;
-  const int rg = t >> 4, dc = t & 15;
-  bf16* dst = tid >= 256 ? s.g : s.q;
-#pragma unroll
-  for (int r4 = 0; r4 < 4; ++r4) st16(&dst[(4 * rg + r4) * kRowStride + 8 * dc], r.x[r4]);
+__device__ __forceinline__ void store_stats(QTileLds& s, const RowStats& r, int tid) {
   if (tid < kBwdRows) {
     s.l2[tid] = r.l2;
     s.dl[tid] = r.dl;
@@ -162,139 +149,128 @@ __device__ __forceinline__ void store_qtile(QTileLds& s, const QTileRegs& r, int
 }  // namespace
 
 __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
-  __shared__ __attribute__((aligned(16))) KvLds sm;
+  __shared__ __attribute__((aligned(16))) QTileLds qs[2];
 
   const BwdTile tile = p.tiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int kw = wave & 3;   // key group
-  const int rh = wave >> 2;  // row half of every query tile
   const int qi = lane & 31;
   const int half = lane >> 5;
   const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
   const int64_t key0 = (int64_t)seq.seg_off + tile.u0;  // first key row in the block
-  const bf16* kbase = p.k_step[tile.step] + key0 * kv_row_stride + tile.kvh * kHeadDim;
-  const bf16* vbase = p.v_step[tile.step] + key0 * kv_row_stride + tile.kvh * kHeadDim;
 
-  // this lane's key (column of S and dP): key 32*kw+qi of the tile
-  const int my_key = 32 * kw + qi;
+  const int tpt = kBwdRows / p.G;  // tokens per query tile
+  const int ntiles = (tile.q_end - tile.q_begin + tpt - 1) / tpt;
+  store_stats(qs[0], fetch_qtile(p, tile, seq, tile.q_begin, tid, qs[0]), tid);
+
+  // this lane's key (column of S and dP): key 32*wave+qi, clamped to the tile
+  const int my_key = 32 * wave + qi;
+  const int kload = my_key < tile.nk ? my_key : tile.nk - 1;
+  bf16x8 kreg[8], vreg[8];
   {
-    const int kk = tid >> 2, qq = tid & 3;  // K and V tiles: key kk, dims 32qq..32qq+31
-    const int u = kk < tile.nk ? kk : tile.nk - 1;
-    const bf16* ksrc = kbase + (int64_t)u * kv_row_stride + 32 * qq;
-    const bf16* vsrc = vbase + (int64_t)u * kv_row_stride + 32 * qq;
+    const bf16* kp = p.k_step[tile.step] + (key0 + kload) * kv_row_stride + tile.kvh * kHeadDim;
+    const bf16* vp = p.v_step[tile.step] + (key0 + kload) * kv_row_stride + tile.kvh * kHeadDim;
 #pragma unroll
-    for (int c8 = 0; c8 < 4; ++c8) {
-      st16(&sm.k[kk * kRowStride + 32 * qq + 8 * c8], ld16(ksrc + 8 * c8));
-      st16(&sm.v[kk * kRowStride + 32 * qq + 8 * c8], ld16(vsrc + 8 * c8));
+    for (int c = 0; c < 8; ++c) {
+      kreg[c] = ld16(kp + 16 * c + 8 * half);
+      vreg[c] = ld16(vp + 16 * c + 8 * half);
     }
   }
-
   f32x16 dk[4], dv[4];
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) {
     dk[nt] = f32x16{};
     dv[nt] = f32x16{};
   }
-
-  const int tpt = kBwdRows / p.G;  // tokens per query tile
-  const int ntiles = (tile.q_end - tile.q_begin + tpt - 1) / tpt;
-  {
-    QTileRegs r;
-    load_qtile(p, tile, seq, tile.q_begin, tid, r);
-    store_qtile(sm.qs[0], r, tid);
-  }
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  const int r0w = 32 * rh;  // first query row of this wavefront inside a tile
-  for (int it = 0; it < ntiles; ++it) {
+  // ---- one query tile on LDS buffer B while tile it+1 is fetched into B^1
+  auto step = [&](int it, auto buf_tag) {
+    constexpr int B = decltype(buf_tag)::value;
+    const QTileLds& cur = qs[B];
     const int qt0 = tile.q_begin + it * tpt;
-    const QTileLds& cur = sm.qs[it & 1];
     const bool more = it + 1 < ntiles;
-    QTileRegs nxt;
-    if (more) load_qtile(p, tile, seq, qt0 + tpt, tid, nxt);  // in flight during the MFMAs below
+    RowStats nst{0.f, 0.f, 0};
+    if (more) nst = fetch_qtile(p, tile, seq, qt0 + tpt, tid, qs[B ^ 1]);
     const bool need_mask =
         qt0 < tile.q_full || qt0 + tpt > tile.q_end || tile.nk < kBwdKeys || tpt * p.G < kBwdRows;
 
-    // ---- S = Q K^T, dP = dO V^T (rows = this wavefront's 32 queries, column = the lane's key)
-    f32x16 s = f32x16{}, dp = f32x16{};
+    auto body = [&](auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
+      // ---- S = Q K^T, dP = dO V^T (rows = queries, column = this lane's key)
+      f32x16 s[2], dp[2];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      s = mfma32(ld16(&cur.q[(r0w + qi) * kRowStride + 16 * c + 8 * half]),
-                 ld16(&sm.k[my_key * kRowStride + 16 * c + 8 * half]), s);
-      dp = mfma32(ld16(&cur.g[(r0w + qi) * kRowStride + 16 * c + 8 * half]),
-                  ld16(&sm.v[my_key * kRowStride + 16 * c + 8 * half]), dp);
-    }
-    // ---- P = exp2(S scale log2e - LSE log2e), dS = P (dP - Delta)
+      for (int mt = 0; mt < 2; ++mt) {
+        s[mt] = f32x16{};
+        dp[mt] = f32x16{};
 #pragma unroll
-    for (int vq = 0; vq < 4; ++vq) {
-      const int r0 = r0w + 8 * vq + 4 * half;
-      const float4 l4 = *reinterpret_cast<const float4*>(&cur.l2[r0]);
-      const float4 d4 = *reinterpret_cast<const float4*>(&cur.dl[r0]);
-      const int4 m4 = *reinterpret_cast<const int4*>(&cur.lim[r0]);
-      const float lr[4] = {l4.x, l4.y, l4.z, l4.w};
-      const float dr[4] = {d4.x, d4.y, d4.z, d4.w};
-      const int mr[4] = {m4.x, m4.y, m4.z, m4.w};
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int v = 4 * vq + c;
-        float pr = fast_exp2(s[v] * p.scale_log2 - lr[c]);
-        if (need_mask && my_key >= mr[c]) pr = 0.f;
-        s[v] = pr;
-        dp[v] = pr * (dp[v] - dr[c]);
+        for (int c = 0; c < 8; ++c) {
+          s[mt] = mfma32(ld16(&cur.q[tile_off<kBwdRows>(32 * mt + qi, 16 * c + 8 * half)]), kreg[c], s[mt]);
+          dp[mt] = mfma32(ld16(&cur.g[tile_off<kBwdRows>(32 * mt + qi, 16 * c + 8 * half)]), vreg[c], dp[mt]);
+        }
       }
-    }
-    // ---- dV += P^T dO, dK += dS^T Q.  k-block t covers rows r0w+16t..+15; a
-    // lane of half h holds rows 16t+4h+{0..3} and 16t+8+4h+{0..3} of it, so
-    // the dO / Q operand is read column-wise from the same rows.
+      // phase fences: reads of a later phase hoisted over this one would
+      // keep their results live across it and exhaust the registers
+      __builtin_amdgcn_sched_barrier(0);
+      // ---- P = exp2(S scale log2e - LSE log2e), dS = P (dP - Delta)
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int v0 = 8 * t;
-      const bf16x8 pa = pack8(s[v0], s[v0 + 1], s[v0 + 2], s[v0 + 3], s[v0 + 4], s[v0 + 5], s[v0 + 6], s[v0 + 7]);
-      const bf16x8 dsa =
-          pack8(dp[v0], dp[v0 + 1], dp[v0 + 2], dp[v0 + 3], dp[v0 + 4], dp[v0 + 5], dp[v0 + 6], dp[v0 + 7]);
-      const int ka = r0w + 16 * t + 4 * half, kb = ka + 8;
+      for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        dv[nt] = mfma32(pa, ld_tr8(cur.g, kRowStride, 32 * nt, ka, kb, lane), dv[nt]);
-        dk[nt] = mfma32(dsa, ld_tr8(cur.q, kRowStride, 32 * nt, ka, kb, lane), dk[nt]);
+        for (int vq = 0; vq < 4; ++vq) {
+          const int r0 = 32 * mt + 8 * vq + 4 * half;
+          const float4 l4 = *reinterpret_cast<const float4*>(&cur.l2[r0]);
+          const float4 d4 = *reinterpret_cast<const float4*>(&cur.dl[r0]);
+          const int4 m4 = *reinterpret_cast<const int4*>(&cur.lim[r0]);
+          const float lr[4] = {l4.x, l4.y, l4.z, l4.w};
+          const float dr[4] = {d4.x, d4.y, d4.z, d4.w};
+          const int mr[4] = {m4.x, m4.y, m4.z, m4.w};
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int v = 4 * vq + c;
+            float pr = fast_exp2(__builtin_fmaf(s[mt][v], p.scale_log2, -lr[c]));
+            if (MASK && my_key >= mr[c]) pr = 0.f;
+            s[mt][v] = pr;
+            dp[mt][v] = pr * (dp[mt][v] - dr[c]);
+          }
+        }
       }
-    }
-    if (more) store_qtile(sm.qs[(it + 1) & 1], nxt, tid);
-    __syncthreads();
-  }
+      __builtin_amdgcn_sched_barrier(0);
+      // ---- dV += P^T dO, dK += dS^T Q.  k-block t covers query rows 16t..16t+15;
+      // a lane of half h holds rows 16t+4h+{0..3} and 16t+8+4h+{0..3} of it, so
+      // the dO / Q operand is read column-wise from the same rows.
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int v0 = 8 * (t & 1);
+        const f32x16& ps = s[t >> 1];
+        const f32x16& dss = dp[t >> 1];
+        const bf16x8 pa =
+            pack8(ps[v0], ps[v0 + 1], ps[v0 + 2], ps[v0 + 3], ps[v0 + 4], ps[v0 + 5], ps[v0 + 6], ps[v0 + 7]);
+        const bf16x8 dsa = pack8(dss[v0], dss[v0 + 1], dss[v0 + 2], dss[v0 + 3], dss[v0 + 4], dss[v0 + 5],
+                                 dss[v0 + 6], dss[v0 + 7]);
+        const int ka = 16 * t + 4 * half, kb = ka + 8;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          dv[nt] = mfma32(pa, ld_tr8<kBwdRows>(cur.g, 32 * nt, ka, kb, lane), dv[nt]);
+          dk[nt] = mfma32(dsa, ld_tr8<kBwdRows>(cur.q, 32 * nt, ka, kb, lane), dk[nt]);
+        }
+      }
+    };
+    if (need_mask) body(std::true_type{});
+    else body(std::false_type{});
 
-  // ---- add the two row halves' partial sums (wavefronts w and w+4), one
-  // accumulator set at a time through the (now idle) query-tile buffers
-  float* red = sm.red + (kw * 64) * 64;
-  if (rh == 1) {
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) red[(16 * nt + v) * 64 + lane] = dk[nt][v];
+    if (more) store_stats(qs[B ^ 1], nst, tid);
+    __builtin_amdgcn_s_waitcnt(0);  // this wavefront's direct loads have landed
+    __syncthreads();
+  };
+  int it = 0;
+  for (; it + 1 < ntiles; it += 2) {
+    step(it, std::integral_constant<int, 0>{});
+    step(it + 1, std::integral_constant<int, 1>{});
   }
-  __syncthreads();
-  if (rh == 0) {
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) dk[nt][v] += red[(16 * nt + v) * 64 + lane];
-  }
-  __syncthreads();
-  if (rh == 1) {
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) red[(16 * nt + v) * 64 + lane] = dv[nt][v];
-  }
-  __syncthreads();
-  if (rh == 1) return;
-#pragma unroll
-  for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) dv[nt][v] += red[(16 * nt + v) * 64 + lane];
+  if (it < ntiles) step(it, std::integral_constant<int, 0>{});
 
   // ---- write dK (scaled) and dV: accumulator column = dim, rows = keys
   void* dkout = p.dk_step[tile.step];
@@ -303,7 +279,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int key = 32 * kw + 8 * (v >> 2) + 4 * half + (v & 3);
+      const int key = 32 * wave + 8 * (v >> 2) + 4 * half + (v & 3);
       if (key < tile.nk) {
         const int64_t idx = (key0 + key) * kv_row_stride + tile.kvh * kHeadDim + 32 * nt + qi;
         store_grad(dkout, idx, dk[nt][v] * p.scale, p.grad_f32);
@@ -318,8 +294,8 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
 // 32*dt + 8*(v/4) + 4*half + v%4.
 template <int MODE>
 __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
-  __shared__ __attribute__((aligned(16))) bf16 ks[kFwdKeys * kRowStride];
-  __shared__ __attribute__((aligned(16))) bf16 vs[kFwdKeys * kRowStride];
+  // [buffer][K, V] plane tiles of 64 keys (see tile_off), double-buffered
+  __shared__ __attribute__((aligned(16))) bf16 kvbuf[2][2][kFwdKeys * kHeadDim];
 
   const FwdTile tile = p.qtiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
@@ -367,67 +343,51 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
   const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
 
   if (MODE != kModeFinal) {
-    for (int i = p.step_first; i < p.step_first + p.step_count; ++i) {
-      const int j = ((p.rank - i) % p.C + p.C) % p.C;
-      const int lim_lo = visible_keys(Pmin, j, p.C, seq.c);
-      const int lim_hi = visible_keys(Pmax, j, p.C, seq.c);
+    // One 64-key tile: S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T.
+    // MASK (compile time) only on tiles crossing some row's causal limit.
+    auto compute = [&](int j, int kv0, const bf16* ks, const bf16* vs, auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
       const int my_lim = valid ? visible_keys(tk.P, j, p.C, seq.c) : 0;
-      const bf16* kbase = p.k_step[j] + (int64_t)seq.seg_off * kv_row_stride + tile.kvh * kHeadDim;
-      const bf16* vbase = p.v_step[j] + (int64_t)seq.seg_off * kv_row_stride + tile.kvh * kHeadDim;
-      for (int kv0 = 0; kv0 < lim_hi; kv0 += kFwdKeys) {
-        {
-          const int kk = tid >> 2, qq = tid & 3;
-          int u = kv0 + kk;
-          u = u < lim_hi ? u : lim_hi - 1;
-          const bf16* ksrc = kbase + (int64_t)u * kv_row_stride + 32 * qq;
-          const bf16* vsrc = vbase + (int64_t)u * kv_row_stride + 32 * qq;
+      f32x16 s[2], dp[2];
 #pragma unroll
-          for (int c8 = 0; c8 < 4; ++c8) {
-            st16(&ks[kk * kRowStride + 32 * qq + 8 * c8], ld16(ksrc + 8 * c8));
-            st16(&vs[kk * kRowStride + 32 * qq + 8 * c8], ld16(vsrc + 8 * c8));
-          }
+      for (int kt = 0; kt < 2; ++kt) {
+        s[kt] = f32x16{};
+        dp[kt] = f32x16{};
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          s[kt] = mfma32(ld16(&ks[tile_off<kFwdKeys>(32 * kt + qi, 16 * c + 8 * half)]), qreg[c], s[kt]);
+          dp[kt] = mfma32(ld16(&vs[tile_off<kFwdKeys>(32 * kt + qi, 16 * c + 8 * half)]), greg[c], dp[kt]);
         }
-        __syncthreads();
-        // ---- S^T = K Q^T and dP^T = V dO^T (two 32-key sub-tiles)
-        f32x16 s[2], dp[2];
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          s[kt] = f32x16{};
-          dp[kt] = f32x16{};
-#pragma unroll
-          for (int c = 0; c < 8; ++c) {
-            s[kt] = mfma32(ld16(&ks[(32 * kt + qi) * kRowStride + 16 * c + 8 * half]), qreg[c], s[kt]);
-            dp[kt] = mfma32(ld16(&vs[(32 * kt + qi) * kRowStride + 16 * c + 8 * half]), greg[c], dp[kt]);
-          }
-        }
-        // ---- dS^T = P^T (dP^T - Delta), P^T = exp2(S^T scale log2e - LSE log2e)
-        const bool need_mask = kv0 + kFwdKeys > lim_lo;
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            float pr = fast_exp2(s[kt][v] * p.scale_log2 - lse2);
-            if (need_mask) {
-              const int u = kv0 + 32 * kt + 8 * (v >> 2) + 4 * half + (v & 3);
-              pr = u < my_lim ? pr : 0.f;
-            }
-            dp[kt][v] = pr * (dp[kt][v] - dlt);
-          }
-        // ---- dQ^T += K^T dS^T: k-block t = keys 16t.. of the tile; the lane's
-        // dS^T values of half h are keys 16t+4h+{0..3}, 16t+8+4h+{0..3}
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const f32x16& src = dp[t >> 1];
-          const int v0 = 8 * (t & 1);
-          const bf16x8 b = pack8(src[v0], src[v0 + 1], src[v0 + 2], src[v0 + 3], src[v0 + 4], src[v0 + 5],
-                                 src[v0 + 6], src[v0 + 7]);
-          const int ka = 16 * t + 4 * half, kb = 16 * t + 8 + 4 * half;
-#pragma unroll
-          for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma32(ld_tr8(ks, kRowStride, 32 * dt, ka, kb, lane), b, dq[dt]);
-        }
-        __syncthreads();
       }
-    }
+      // ---- dS^T = P^T (dP^T - Delta), P^T = exp2(S^T scale log2e - LSE log2e)
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          float pr = fast_exp2(__builtin_fmaf(s[kt][v], p.scale_log2, -lse2));
+          if (MASK) {
+            const int u = kv0 + 32 * kt + 8 * (v >> 2) + 4 * half + (v & 3);
+            pr = u < my_lim ? pr : 0.f;
+          }
+          dp[kt][v] = pr * (dp[kt][v] - dlt);
+        }
+      // ---- dQ^T += K^T dS^T: k-block t = keys 16t.. of the tile; the lane's
+      // dS^T values of half h are keys 16t+4h+{0..3}, 16t+8+4h+{0..3}
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const f32x16& src = dp[t >> 1];
+        const int v0 = 8 * (t & 1);
+        const bf16x8 b = pack8(src[v0], src[v0 + 1], src[v0 + 2], src[v0 + 3], src[v0 + 4], src[v0 + 5],
+                               src[v0 + 6], src[v0 + 7]);
+        const int ka = 16 * t + 4 * half, kb = ka + 8;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma32(ld_tr8<kFwdKeys>(ks, 32 * dt, ka, kb, lane), b, dq[dt]);
+      }
+    };
+    walk_kv_tiles(p, seq, tile.kvh, Pmax, wave, lane, kvbuf, [&](int j, int kv0, const bf16* ks, const bf16* vs) {
+      if (kv0 + kFwdKeys <= visible_keys(Pmin, j, p.C, seq.c)) compute(j, kv0, ks, vs, std::false_type{});
+      else compute(j, kv0, ks, vs, std::true_type{});
+    });
   }
 
   if (MODE == kModeStep) {

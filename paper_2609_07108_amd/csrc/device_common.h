@@ -53,16 +53,58 @@ __device__ __forceinline__ bf16x4 ld_tr4(const bf16* p) {
   return __builtin_bit_cast(bf16x4, r);
 }
 
-// MFMA operand (8 reduction values per lane) read column-wise from a
-// row-major LDS tile T (row stride `rs` elements): lane l takes column
-// n0 + l%32; its reduction slots 0..3 come from rows ka..ka+3 and slots 4..7
-// from rows kb..kb+3 (ka, kb may depend on the lane's half l/32).
-__device__ __forceinline__ bf16x8 ld_tr8(const bf16* T, int rs, int n0, int ka, int kb, int lane) {
+// Direct global -> LDS copy (global_load_lds_dwordx4): lane i of the
+// wavefront reads 16 bytes at `src` and the hardware writes them to
+// lds_base + 16*i; lds_base must be the same for every lane.  Completion is
+// tracked by the vector-memory counter.
+__device__ __forceinline__ void dma16(const void* src, void* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(lds_base), 16, 0, 0);
+}
+
+// LDS tiles of R rows x 128 bf16 columns (one head) are stored as four
+// 32-column planes, plane-major: plane p holds columns 32p..32p+31 of every
+// row, 64 bytes per row, and the four 16-byte chunks of row r inside a plane
+// are XOR-permuted by (r/4)%4.  With 64 LDS banks (256 bytes per cycle):
+//  * 16-byte row reads (MFMA operands, 16 lanes = 16 aligned rows at one
+//    column chunk) hit bank group 4*(r%4) + (chunk ^ (r/4)%4): 16 distinct;
+//  * 8-byte transposed reads (ds_read_b64_tr_b16, 32 lanes = 4 aligned rows
+//    x 32 columns of one plane) cover 256 contiguous bytes;
+//  * a direct global-to-LDS load (64 lanes x 16 bytes, contiguous) fills 16
+//    rows of one plane.
+// Moving to another plane, or to rows 16 further down, only adds a constant
+// to the address, so one base register serves many reads.
+template <int R>
+__device__ __forceinline__ int tile_off(int r, int c) {
+  return (((c >> 5) * R + r) << 5) + (((((c >> 3) & 3) ^ ((r >> 2) & 3))) << 3) + (c & 7);
+}
+
+// MFMA operand (8 reduction values per lane) read column-wise from a plane
+// tile T[k][n] of R rows: lane l takes column n0 + l%32 (n0 a multiple of 32);
+// its reduction slots 0..3 come from rows ka..ka+3 and slots 4..7 from rows
+// kb..kb+3 (ka, kb multiples of 4; they may depend on the lane's half l/32).
+template <int R>
+__device__ __forceinline__ bf16x8 ld_tr8(const bf16* T, int n0, int ka, int kb, int lane) {
   const int i = lane & 15;
   const int col = n0 + (lane & 16) + 4 * (i & 3);
-  const bf16x4 lo = ld_tr4(T + (ka + (i >> 2)) * rs + col);
-  const bf16x4 hi = ld_tr4(T + (kb + (i >> 2)) * rs + col);
+  const bf16x4 lo = ld_tr4(T + tile_off<R>(ka + (i >> 2), col));
+  const bf16x4 hi = ld_tr4(T + tile_off<R>(kb + (i >> 2), col));
   return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Direct load of rows into a plane tile of R rows: instruction m of a
+// fetch (m = 0 .. R/4 - 1) fills rows 16*(m/4).. of plane m%4; lane i of it
+// carries row 16*(m/4) + i/4 and the logical 8-column chunk returned by
+// dma_col.  The caller supplies the row's global address.
+template <int R>
+__device__ __forceinline__ int dma_row(int m, int lane) { return 16 * (m >> 2) + (lane >> 2); }
+template <int R>
+__device__ __forceinline__ int dma_col(int m, int lane) {
+  const int row = dma_row<R>(m, lane);
+  return 32 * (m & 3) + 8 * ((lane & 3) ^ ((row >> 2) & 3));
+}
+template <int R>
+__device__ __forceinline__ bf16* dma_dst(bf16* T, int m) {
+  return T + (((m & 3) * R + 16 * (m >> 2)) << 5);
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

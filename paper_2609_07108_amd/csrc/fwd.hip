@@ -9,10 +9,13 @@
 //                      with the other half-wavefront)
 //   online softmax    (exp2 domain, fp32 statistics)
 //   O^T += V^T P^T    (P^T taken straight from the S^T accumulator registers;
-//                      V^T staged in LDS with the matching key permutation)
+//                      V^T read column-wise from the row-major V tile with
+//                      transposing LDS reads, in the matching key order)
 // Tiles that are fully visible to every row skip the mask; the causal limit
 // of a row in block j is a prefix of the block because positions increase
-// with the local index (chunk j, then chunk 2C-1-j).
+// with the local index (chunk j, then chunk 2C-1-j).  K and V tiles arrive by
+// direct global-to-LDS loads, double-buffered across ring steps
+// (walk_kv_tiles), so the next tile is in flight during the MFMAs.
 //
 // Epilogues
 //   STEP  : merge the step's partial (O, LSE) into the running fp32 pair in
@@ -23,6 +26,8 @@
 // (chain members 0..i, or the whole block; at most 64 keys, on the vector
 // ALUs), merge it with the main partial by Eq. lse-merge and write bf16 O and
 // the natural-log LSE.
+#include <type_traits>
+
 #include "ba_internal.h"
 #include "device_common.h"
 #include "kernels.h"
@@ -30,17 +35,6 @@
 namespace ba {
 
 namespace {
-
-constexpr int kKStride = kHeadDim + 8;  // padded K tile row (elements)
-
-// V^T tile: 128 rows (head dim) x 64 keys, 8 chunks of 16 bytes per row.
-// Logical chunk 2t+h holds keys 16t+4h+{0..3} then 16t+8+4h+{0..3}: exactly
-// the keys a lane of half h contributes to PV k-block t from its S^T
-// accumulator.  Chunks are XOR-swizzled per row against bank conflicts.
-__device__ __forceinline__ int vt_index(int d, int lchunk) {
-  const int sw = (d ^ (d >> 3)) & 7;
-  return d * kFwdKeys + ((lchunk ^ sw) << 3);
-}
 
 struct RowState {
   f32x16 o[4];  // O^T accumulator, d = 32*dt + 8*(v/4) + 4*half + v%4
@@ -52,8 +46,8 @@ struct RowState {
 
 template <int MODE>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
-  __shared__ __attribute__((aligned(16))) bf16 ks[kFwdKeys * kKStride];
-  __shared__ __attribute__((aligned(16))) bf16 vt[kHeadDim * kFwdKeys];
+  // [buffer][K, V] plane tiles of 64 keys (see tile_off), double-buffered
+  __shared__ __attribute__((aligned(16))) bf16 kvbuf[2][2][kFwdKeys * kHeadDim];
 
   const FwdTile tile = p.tiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
@@ -90,107 +84,74 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
 
   if (MODE != kModeFinal) {
-    for (int i = p.step_first; i < p.step_first + p.step_count; ++i) {
-      const int j = ((p.rank - i) % p.C + p.C) % p.C;
-      const int lim_lo = visible_keys(Pmin, j, p.C, seq.c);
-      const int lim_hi = visible_keys(Pmax, j, p.C, seq.c);
+    // One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.  MASK
+    // (compile time) only on tiles crossing some row's causal limit.
+    auto compute = [&](int j, int kv0, const bf16* ks, const bf16* vs, auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
       const int my_lim = valid ? visible_keys(tk.P, j, p.C, seq.c) : 0;
-      const bf16* kbase = p.k_step[j] + (int64_t)seq.seg_off * kv_row_stride + tile.kvh * kHeadDim;
-      const bf16* vbase = p.v_step[j] + (int64_t)seq.seg_off * kv_row_stride + tile.kvh * kHeadDim;
-
-      for (int kv0 = 0; kv0 < lim_hi; kv0 += kFwdKeys) {
-        // ---- stage K (row-major, padded) and V^T (permuted, swizzled) in LDS
-        {
-          const int kk = tid >> 2, qq = tid & 3;
-          int u = kv0 + kk;
-          u = u < lim_hi ? u : lim_hi - 1;
-          const bf16* src = kbase + (int64_t)u * kv_row_stride + 32 * qq;
+      // ---- S^T = K Q^T : two 32-key sub-tiles
+      f32x16 s[2];
 #pragma unroll
-          for (int c8 = 0; c8 < 4; ++c8) st16(&ks[kk * kKStride + 32 * qq + 8 * c8], ld16(src + 8 * c8));
-        }
-        {
-          const int kg = tid >> 4, dc = tid & 15;
-          bf16x8 v4[4];
+      for (int kt = 0; kt < 2; ++kt) {
+        s[kt] = f32x16{};
 #pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4) {
-            int u = kv0 + 4 * kg + r4;
-            u = u < lim_hi ? u : lim_hi - 1;
-            v4[r4] = ld16(vbase + (int64_t)u * kv_row_stride + 8 * dc);
+        for (int ks8 = 0; ks8 < 8; ++ks8)
+          s[kt] = mfma32(ld16(&ks[tile_off<kFwdKeys>(32 * kt + qi, 16 * ks8 + 8 * half)]), qreg[ks8], s[kt]);
+      }
+      // ---- online softmax in the log2 domain; the scale is positive, so
+      // the row maximum is taken on raw scores and applied once
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          if (MASK) {
+            const int u = kv0 + 32 * kt + 8 * (v >> 2) + 4 * half + (v & 3);
+            s[kt][v] = u < my_lim ? s[kt][v] : -INFINITY;
           }
-          const int tb = kg >> 2, a = (kg & 3) >> 1, b = kg & 1;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int d = 8 * dc + e;
-            bf16x4 w;
-            w[0] = v4[0][e]; w[1] = v4[1][e]; w[2] = v4[2][e]; w[3] = v4[3][e];
-            *reinterpret_cast<bf16x4*>(&vt[vt_index(d, 2 * tb + b) + 4 * a]) = w;
-          }
+          mx = fmaxf(mx, s[kt][v]);
         }
-        __syncthreads();
-
-        // ---- S^T = K Q^T : two 32-key sub-tiles
-        f32x16 s[2];
+      }
+      mx = fmaxf(mx, xor32(mx)) * p.scale_log2;
+      const float m_new = fmaxf(st.m, mx);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = fast_exp2(st.m - m_use);
+      float lsum = 0.f;
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          s[kt] = f32x16{};
+      for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
-          for (int ks8 = 0; ks8 < 8; ++ks8)
-            s[kt] = mfma32(ld16(&ks[(32 * kt + qi) * kKStride + 16 * ks8 + 8 * half]), qreg[ks8], s[kt]);
+        for (int v = 0; v < 16; ++v) {
+          const float e = fast_exp2(__builtin_fmaf(s[kt][v], p.scale_log2, -m_use));
+          s[kt][v] = e;
+          lsum += e;
         }
-
-        // ---- online softmax (log2 domain)
-        const bool need_mask = kv0 + kFwdKeys > lim_lo;
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            float x = s[kt][v] * p.scale_log2;
-            if (need_mask) {
-              const int u = kv0 + 32 * kt + 8 * (v >> 2) + 4 * half + (v & 3);
-              x = u < my_lim ? x : -INFINITY;
-            }
-            s[kt][v] = x;
-            mx = fmaxf(mx, x);
-          }
-        }
-        mx = fmaxf(mx, xor32(mx));
-        const float m_new = fmaxf(st.m, mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = fast_exp2(st.m - m_use);
-        float lsum = 0.f;
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float e = fast_exp2(s[kt][v] - m_use);
-            s[kt][v] = e;
-            lsum += e;
-          }
-        }
-        st.l = st.l * alpha + lsum;
-        st.m = m_new;
+      }
+      st.l = st.l * alpha + lsum;
+      st.m = m_new;
+      // the running output only needs rescaling when some row's maximum grew
+      if (__ballot(alpha != 1.f)) {
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) st.o[dt] *= alpha;
-
-        // ---- O^T += V^T P^T : k-block t uses keys 16t.. of the tile
-        bf16x8 pb[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const f32x16& src = s[t >> 1];
-          const int v0 = 8 * (t & 1);
-          pb[t] = pack8(src[v0], src[v0 + 1], src[v0 + 2], src[v0 + 3], src[v0 + 4], src[v0 + 5],
-                        src[v0 + 6], src[v0 + 7]);
-        }
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) {
-#pragma unroll
-          for (int t = 0; t < 4; ++t)
-            st.o[dt] = mfma32(ld16(&vt[vt_index(32 * dt + qi, 2 * t + half)]), pb[t], st.o[dt]);
-        }
-        __syncthreads();
       }
-    }
+      // ---- O^T += V^T P^T : k-block t = keys 16t.. of the tile; a lane of
+      // half h holds keys 16t+4h+{0..3} and 16t+8+4h+{0..3} of it in its S^T
+      // registers, and reads the V^T operand from exactly those key rows
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const f32x16& src = s[t >> 1];
+        const int v0 = 8 * (t & 1);
+        const bf16x8 pb = pack8(src[v0], src[v0 + 1], src[v0 + 2], src[v0 + 3], src[v0 + 4], src[v0 + 5],
+                                src[v0 + 6], src[v0 + 7]);
+        const int ka = 16 * t + 4 * half, kb = ka + 8;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+          st.o[dt] = mfma32(ld_tr8<kFwdKeys>(vs, 32 * dt, ka, kb, lane), pb, st.o[dt]);
+      }
+    };
+    walk_kv_tiles(p, seq, tile.kvh, Pmax, wave, lane, kvbuf, [&](int j, int kv0, const bf16* ks, const bf16* vs) {
+      if (kv0 + kFwdKeys <= visible_keys(Pmin, j, p.C, seq.c)) compute(j, kv0, ks, vs, std::false_type{});
+      else compute(j, kv0, ks, vs, std::true_type{});
+    });
   }
 
   // ------------------------------------------------------------ epilogues

@@ -77,6 +77,75 @@ struct BwdParams {
   float* dq_acc;    // [T * hq, d] running unscaled dS K sums (per-step schedule)
 };
 
+// Walk over the 64-key tiles of every ring step in [step_first,
+// step_first + step_count) that a query tile with largest causal limit Pmax
+// can see.  Each tile's K and V rows are fetched with direct global-to-LDS
+// loads into plane tiles (see tile_off), double-buffered: while `body`
+// computes on one buffer the next tile, possibly of the next ring step, is
+// already in flight into the other.  The buffers are used in a fixed
+// alternation so their LDS addresses are compile-time constants in the body.
+// body(j, kv0, ks, vs) is called once per tile with the ring block j, the
+// first key kv0 (index inside the sequence's segment of block j) and the
+// staged K and V tiles; rows past the block's visible prefix hold clamped
+// copies and must be masked by the body.
+struct KvCursor {
+  int i, j, kv0, lim_hi;
+};
+
+template <class P, class Body>
+__device__ __forceinline__ void walk_kv_tiles(const P& p, const SeqInfo& seq, int kvh, int Pmax, int wave,
+                                              int lane, bf16 (&kv)[2][2][kFwdKeys * kHeadDim], Body&& body) {
+  const int step_end = p.step_first + p.step_count;
+  const int64_t stride = (int64_t)p.hkv * kHeadDim;
+  auto seek = [&](int i) {
+    KvCursor c{i, 0, 0, 0};
+    for (; c.i < step_end; ++c.i) {
+      c.j = ((p.rank - c.i) % p.C + p.C) % p.C;  // ring step i brings rank (r - i) mod C
+      c.lim_hi = visible_keys(Pmax, c.j, p.C, seq.c);
+      if (c.lim_hi > 0) break;
+    }
+    return c;
+  };
+  auto next = [&](KvCursor c) {
+    c.kv0 += kFwdKeys;
+    return c.kv0 < c.lim_hi ? c : seek(c.i + 1);
+  };
+  auto fetch = [&](const KvCursor& c, bf16* kd, bf16* vd) {
+    const bf16* kb = p.k_step[c.j] + (int64_t)seq.seg_off * stride + kvh * kHeadDim;
+    const bf16* vb = p.v_step[c.j] + (int64_t)seq.seg_off * stride + kvh * kHeadDim;
+#pragma unroll
+    for (int m4 = 0; m4 < 4; ++m4) {
+      const int m = 4 * wave + m4;  // 16 loads per tensor and tile, 4 per wavefront
+      int u = c.kv0 + dma_row<kFwdKeys>(m, lane);
+      u = u < c.lim_hi ? u : c.lim_hi - 1;
+      const int col = dma_col<kFwdKeys>(m, lane);
+      dma16(kb + (int64_t)u * stride + col, dma_dst<kFwdKeys>(kd, m));
+      dma16(vb + (int64_t)u * stride + col, dma_dst<kFwdKeys>(vd, m));
+    }
+  };
+  KvCursor cur = seek(p.step_first);
+  if (cur.i >= step_end) return;
+  fetch(cur, kv[0][0], kv[0][1]);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  while (true) {
+    KvCursor nx = next(cur);
+    if (nx.i < step_end) fetch(nx, kv[1][0], kv[1][1]);
+    body(cur.j, cur.kv0, kv[0][0], kv[0][1]);
+    __builtin_amdgcn_s_waitcnt(0);  // this wavefront's loads of the next tile have landed
+    __syncthreads();
+    if (nx.i >= step_end) return;
+    cur = nx;
+    nx = next(cur);
+    if (nx.i < step_end) fetch(nx, kv[0][0], kv[0][1]);
+    body(cur.j, cur.kv0, kv[1][0], kv[1][1]);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (nx.i >= step_end) return;
+    cur = nx;
+  }
+}
+
 hipError_t launch_fwd(const FwdParams& p, int mode, hipStream_t stream);
 hipError_t launch_bwd_preprocess(const BwdParams& p, hipStream_t stream);
 hipError_t launch_bwd_kv(const BwdParams& p, hipStream_t stream);

@@ -83,7 +83,8 @@ static int build_plan(const ba_problem* pr, Plan& P) {
   const int32_t G = pr->hq / pr->hkv;
   if (G > kBwdRows)
     return fail(BA_E_UNSUPPORTED, "hq/hkv > " + std::to_string(kBwdRows) + " unsupported");
-  if (!std::isfinite(pr->softmax_scale)) return fail(BA_E_INVAL, "softmax_scale not finite");
+  if (!std::isfinite(pr->softmax_scale) || pr->softmax_scale <= 0.f)
+    return fail(BA_E_INVAL, "softmax_scale must be finite and positive");
   if (pr->num_groups < 0 || (pr->num_groups > 0 && !pr->groups))
     return fail(BA_E_INVAL, "groups missing");
   if (pr->num_branch_rows < 0) return fail(BA_E_INVAL, "num_branch_rows < 0");
