@@ -165,3 +165,22 @@ def test_errors_do_not_launch(cuda):
                           share.t["v_br"], share.t["k_step"], share.t["v_step"], misaligned, out["o_br"],
                           out["lse_main"], out["lse_br"], RS.workspace(share, B.BA_MODE_FUSED))
     assert e.value.code == B.BA_E_INVAL
+
+
+def test_share_without_queries(cuda):
+    """A rank share with main keys but no query token (a DFlash-only sequence
+    whose blocks all sit on other ranks): both calls succeed and the per-step
+    key gradients come back zero."""
+    prob = W.custom([128], [("dflash", 4, 64)], hq=2, hkv=1, cp_size=2, cp_rank=0, seed=206, anchor_seed=7)
+    prob.g_anchor[:] = 40  # chunk 1 of 4 -> rank 1
+    share = RS.build_share(prob, device="cuda")
+    assert share.plan.info()[1] == 0
+    out = RS.alloc_outputs(share, grads=True)
+    for x in out["dk_step"] + out["dv_step"]:
+        x.fill_(1.0)
+    ws = RS.workspace(share, B.BA_MODE_FUSED, backward=True)
+    RS.run_fwd(share, out, B.BA_MODE_FUSED, ws)
+    RS.run_bwd(share, out, B.BA_MODE_FUSED, ws)
+    torch.cuda.synchronize()
+    for x in out["dk_step"] + out["dv_step"]:
+        assert torch.count_nonzero(x).item() == 0
