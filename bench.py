@@ -37,15 +37,17 @@ PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/c
 # calibration (profiles/traffic_eagle3-K3-L262144-cp8r0.md).  A figure only
 # applies while the kernel's source is the one that was measured.
 MEASURED_TRAFFIC = {
-    "bwd_kv_kernel": {"source": "bwd.hip", "sha256_16": "e495667509d65906", "bytes": 189371247257},
-    "bwd_dq_kernel": {"source": "bwd.hip", "sha256_16": "e495667509d65906", "bytes": 1879061264353},
-    "fwd_kernel": {"source": "fwd.hip", "sha256_16": "d22e737329a6928d", "bytes": 688617242893},
+    ("bwd_kv_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "e495667509d65906", "bytes": 189371247257},
+    ("bwd_dq_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "e495667509d65906", "bytes": 1879061264353},
+    ("fwd_kernel", "fused"): {"source": "fwd.hip", "sha256_16": "d22e737329a6928d", "bytes": 688617242893},
 }
 
 
-def measured_traffic(kernel: str, workload: str):
+def measured_traffic(kernel: str, workload: str, mode: str):
+    """HBM bytes per launch of `kernel`, or None if not measured for this
+    workload and schedule or if the kernel changed since."""
     import hashlib
-    m = MEASURED_TRAFFIC.get(kernel)
+    m = MEASURED_TRAFFIC.get((kernel, mode))
     if m is None or workload != "eagle3-K3-L262144-cp8r0":
         return None
     path = os.path.join(ROOT, "paper_2609_07108_amd", "csrc", m["source"])
@@ -137,7 +139,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4, help="named workload 1..5 (4 = 256K headline)")
-    ap.add_argument("--mode", choices=["fused", "per_step"], default="fused")
+    ap.add_argument("--mode", choices=["fused", "per_step"], default="per_step",
+                    help="per_step: one launch per ring step (the ring's schedule); fused: one walk over all blocks")
     ap.add_argument("--cpu-rows", type=int, default=24, help="oracle sample size (0 disables)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB mebibytes (HBM counter calibration)")
@@ -207,15 +210,13 @@ def main():
     ms_step = total_ms / args.steps
     fwd_ring_ms = sum(ev.ms(a, b) for a, b in zip(fb, fe)) / args.steps
     bwd_ring_ms = sum(ev.ms(a, b) for a, b in zip(bb, be)) / args.steps
-    kern = {"fwd_kernel": (fwd_ring_ms, ring_fwd_flops)}
-    if mode == B.BA_MODE_FUSED:
-        # the backward ring part is two kernels: dK/dV (S, dP, dV, dK: 8d per
-        # pair) then dQ (S, dP, dQ: 6d per pair)
-        kv_ms = sum(ev.ms(a, b) for a, b in zip(bb, bk)) / args.steps
-        kern["bwd_kv_kernel"] = (kv_ms, main_pairs * hq * 8 * d)
-        kern["bwd_dq_kernel"] = (bwd_ring_ms - kv_ms, main_pairs * hq * 6 * d)
-    else:
-        kern["bwd ring (dK/dV + dQ)"] = (bwd_ring_ms, main_pairs * hq * 14 * d)
+    # the backward ring part is two kernels: dK/dV (S, dP, dV, dK: 8d per
+    # pair) then dQ (S, dP, dQ: 6d per pair); in the per-step schedule each
+    # is C launches, so time per launch and FLOPs per launch scale alike
+    kv_ms = sum(ev.ms(a, b) for a, b in zip(bb, bk)) / args.steps
+    kern = {"fwd_kernel": (fwd_ring_ms, ring_fwd_flops),
+            "bwd_kv_kernel": (kv_ms, main_pairs * hq * 8 * d),
+            "bwd_dq_kernel": (bwd_ring_ms - kv_ms, main_pairs * hq * 6 * d)}
     print(f"[bench] {args.steps} steps: {ms_step:.2f} ms/step; " +
           ", ".join(f"{k} {v[0]:.2f} ms ({v[1] / v[0] / 1e9:.0f} TFLOP/s)" for k, v in kern.items()),
           file=sys.stderr, flush=True)
@@ -232,6 +233,7 @@ def main():
         cpu = cpu_baseline(prob, args.cpu_rows)
 
     n_local, ntok = share.plan.info()
+    traffic = measured_traffic(dom_name, prob.name, args.mode)
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak",
@@ -246,7 +248,7 @@ def main():
         "roofline": {"kernel": dom_name, "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": round(PEAK_BF16_TFLOPS, 1), "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic(dom_name, prob.name),
+                     "traffic": traffic,
                      "launches_per_step": launches},
         "cpu_baseline": cpu,
     }

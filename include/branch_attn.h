@@ -142,8 +142,9 @@ typedef struct ba_fwd_io {
  * k_step[j] (the gradient contributed by THIS rank's queries to rank j's
  * block; a real ring returns it to rank j), dk_br / dv_br like k_br.  The
  * LSE outputs receive no gradient.  ring_begin / ring_end as in ba_fwd_io;
- * kv_end (optional hipEvent_t) is recorded in BA_MODE_FUSED between the
- * dK/dV launch and the dQ launch of the ring part, and ignored otherwise. */
+ * kv_end (optional hipEvent_t) is recorded between the dK/dV launches and
+ * the dQ launches of the ring part (in BA_MODE_PER_STEP all C dK/dV steps
+ * are launched before the C dQ steps). */
 typedef struct ba_bwd_io {
   const void* q_main;
   const void* q_br;

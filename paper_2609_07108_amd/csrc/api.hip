@@ -228,6 +228,8 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
   p.dv_br = io->dv_br;
   p.grad_f32 = io->grad_dtype == BA_DTYPE_F32;
   p.rowstat = reinterpret_cast<float2*>(c.ws + c.w.rowstat);
+  p.qtok = reinterpret_cast<bf16*>(c.ws + c.w.qtok);
+  p.gtok = reinterpret_cast<bf16*>(c.ws + c.w.gtok);
   p.dq_acc = mode == BA_MODE_PER_STEP ? reinterpret_cast<float*>(c.ws + c.w.dq_acc) : nullptr;
 
   if ((e = launch_bwd_preprocess(p, stream)) != hipSuccess) return hip_fail(e, "preprocess launch");
@@ -243,11 +245,17 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
     if ((e = launch_bwd_dq(p, kModeFused, stream)) != hipSuccess) return hip_fail(e, "dQ launch");
     if ((e = record(io->ring_end, stream)) != hipSuccess) return hip_fail(e, "event record");
   } else {
-    // ring replay: per step, dK/dV of the arriving block and this rank's dQ sums
+    // ring replay: per ring step, dK/dV of the arriving block (returned to its
+    // owner in a real ring), then per step this rank's dQ sums.  The two
+    // launch sequences are independent, so the dK/dV steps go first and the
+    // dQ steps after them.
     for (int i = 0; i < P.cp_size; ++i) {
       p.tiles = tiles + P.bwd_step_off[i];
       p.num_tiles = P.bwd_step_off[i + 1] - P.bwd_step_off[i];
       if ((e = launch_bwd_kv(p, stream)) != hipSuccess) return hip_fail(e, "ring-step dK/dV launch");
+    }
+    if ((e = record(io->kv_end, stream)) != hipSuccess) return hip_fail(e, "event record");
+    for (int i = 0; i < P.cp_size; ++i) {
       p.step_first = i;
       p.step_count = 1;
       p.acc_first = i == 0;

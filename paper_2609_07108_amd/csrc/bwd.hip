@@ -46,8 +46,9 @@ __device__ __forceinline__ void store_grad(void* base, int64_t idx, float v, boo
 }  // namespace
 
 // ------------------------------------------------------------ preprocess
-// 32 lanes per (token, head): Delta = <dO, O> over 128 dims, and the row's
-// LSE in log2 units.
+// 32 lanes per (token, head): Delta = <dO, O> over 128 dims and the row's
+// LSE in log2 units; Q and dO rows are also copied into token order, so the
+// dK/dV kernel addresses a query tile without indirection.
 __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
   const int64_t pair = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 5;
   const int sub = threadIdx.x & 31;
@@ -59,6 +60,9 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
   const bf16* g = row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head);
   const bf16x4 ov = reinterpret_cast<const bf16x4*>(o)[sub];
   const bf16x4 gv = reinterpret_cast<const bf16x4*>(g)[sub];
+  const bf16x4 qv = reinterpret_cast<const bf16x4*>(row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head))[sub];
+  reinterpret_cast<bf16x4*>(p.qtok + pair * kHeadDim)[sub] = qv;
+  reinterpret_cast<bf16x4*>(p.gtok + pair * kHeadDim)[sub] = gv;
   float dlt = (float)ov[0] * (float)gv[0] + (float)ov[1] * (float)gv[1] + (float)ov[2] * (float)gv[2] +
               (float)ov[3] * (float)gv[3];
 #pragma unroll
@@ -71,85 +75,43 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------ kv (ring)
-// Workgroup of 4 wavefronts (one per SIMD, so up to 512 registers each) on
-// 128 keys: wavefront w owns keys 32w..32w+31 against every 64-row query
-// tile.  K and V of its keys stay in registers (B operands of S = Q K^T and
-// dP = dO V^T), dK and dV accumulate in registers.  Query tiles (Q and dO)
-// are double-buffered plane tiles (see tile_off) fetched with direct
-// global-to-LDS loads while the previous one is in use; the loop is unrolled
-// by two so that each half works on a fixed buffer.
+// Workgroup of 4 wavefronts (one per SIMD, up to 512 registers each) on 128
+// keys: wavefront w owns keys 32w..32w+31 against every 64-row query tile
+// (tokens x the G heads of the KV head).  K and V of its keys stay in
+// registers (B operands of S = Q K^T and dP = dO V^T), dK and dV accumulate
+// in registers.  No atomics.
+//
+// Query tiles (Q and dO plane tiles plus per-row LSE, Delta and causal
+// limit) rotate through three LDS buffers: while tile i is processed, tile
+// i+1 is resident and tile i+2 in flight.  Every global access of the loop
+// is such a direct load, at addresses computed from the token index alone
+// (token-ordered copies of Q and dO), so the loop has no compiler-visible
+// memory loads and the waits on the loads are explicit.
+//
+// Inside a stage the 64 MFMAs run in a fixed order -- S/dP of row block 0,
+// S/dP of row block 1, dV/dK over the four 16-row reduction blocks -- each
+// preceded by the LDS read of the operand kOpAhead MFMAs later and, from
+// the 17th on, by one softmax element, so that the exponentials overlap the
+// matrix work and no LDS latency is exposed.
 namespace {
 
 constexpr int kKvWaves = 4;
 constexpr int kKvThreads = 64 * kKvWaves;
+constexpr int kOpAhead = 4;
+constexpr int kDmaPerStage = 8;  // Q/dO direct loads of one wavefront per tile
 
 struct QTileLds {
   bf16 q[kBwdRows * kHeadDim];
   bf16 g[kBwdRows * kHeadDim];
-  float l2[kBwdRows];
-  float dl[kBwdRows];
-  int lim[kBwdRows];
+  float l2[kBwdRows];  // LSE * log2 e
+  float dl[kBwdRows];  // Delta
+  int pl[kBwdRows];    // causal limit P (-1: no token)
 };
-
-struct RowStats {
-  float l2, dl;
-  int lim;
-};
-
-// Issue the direct loads of the query tile starting at token qt0 into `s`:
-// wavefronts 0-1 fetch Q, 2-3 dO, eight loads of 16 rows x 32 columns each.
-// Rows without a token (past the range, or past tpt*G) fetch the tile's
-// first row: their probabilities are masked to zero, so only finiteness
-// matters.  Threads 0..63 also return the row statistics, written to LDS
-// once the buffer is no longer read.
-__device__ __forceinline__ RowStats fetch_qtile(const BwdParams& p, const BwdTile& tile, const SeqInfo& seq,
-                                               int qt0, int tid, QTileLds& s) {
-  const int G = p.G;
-  const int tpt = kBwdRows / G;
-  const int lane = tid & 63, wave = tid >> 6;
-  const bool is_do = wave >= 2;
-  const bf16* mainp = is_do ? p.do_main : p.q_main;
-  const bf16* brp = is_do ? p.do_br : p.q_br;
-  bf16* dst = is_do ? s.g : s.q;
-#pragma unroll
-  for (int m8 = 0; m8 < 8; ++m8) {
-    const int m = 8 * (wave & 1) + m8;
-    const int row = dma_row<kBwdRows>(m, lane);
-    const int tl = row / G;
-    const int tok = qt0 + tl;
-    const bool ok = tl < tpt && tok < tile.q_end;
-    const TokInfo tk = p.toks[ok ? tok : qt0];
-    const int head = tile.kvh * G + (ok ? row - tl * G : 0);
-    dma16(row_ptr(mainp, brp, tk.qrow, p.hq, head) + dma_col<kBwdRows>(m, lane), dma_dst<kBwdRows>(dst, m));
-  }
-  RowStats r{0.f, 0.f, 0};
-  if (tid < kBwdRows) {
-    const int tl = tid / G;
-    const int tok = qt0 + tl;
-    if (tl < tpt && tok < tile.q_end) {
-      const int head = tile.kvh * G + (tid - tl * G);
-      const float2 rs = p.rowstat[(int64_t)tok * p.hq + head];
-      r.l2 = rs.x;
-      r.dl = rs.y;
-      const int lim = visible_keys(p.toks[tok].P, tile.step, p.C, seq.c) - tile.u0;
-      r.lim = lim < tile.nk ? lim : tile.nk;
-    }
-  }
-  return r;
-}
-
-__device__ __forceinline__ void store_stats(QTileLds& s, const RowStats& r, int tid) {
-  if (tid < kBwdRows) {
-    s.l2[tid] = r.l2;
-    s.dl[tid] = r.dl;
-    s.lim[tid] = r.lim;
-  }
-}
 
 }  // namespace
 
 __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
-  __shared__ __attribute__((aligned(16))) QTileLds qs[2];
+  __shared__ __attribute__((aligned(16))) QTileLds qs[3];
 
   const BwdTile tile = p.tiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
@@ -158,16 +120,64 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   const int wave = tid >> 6;
   const int qi = lane & 31;
   const int half = lane >> 5;
+  const int G = p.G;
+  const int tpt = kBwdRows / G;  // tokens per query tile
+  const int ntiles = (tile.q_end - tile.q_begin + tpt - 1) / tpt;  // >= 1 (planner)
   const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
   const int64_t key0 = (int64_t)seq.seg_off + tile.u0;  // first key row in the block
+  const int head0 = tile.kvh * G;
 
-  const int tpt = kBwdRows / p.G;  // tokens per query tile
-  const int ntiles = (tile.q_end - tile.q_begin + tpt - 1) / tpt;
-  store_stats(qs[0], fetch_qtile(p, tile, seq, tile.q_begin, tid, qs[0]), tid);
-
-  // this lane's key (column of S and dP): key 32*wave+qi, clamped to the tile
+  // ---- this lane's key: its position decides visibility (visible to a row
+  // iff position <= the row's causal limit; local index < c lies in chunk
+  // `step`, the rest in chunk 2C-1-step)
   const int my_key = 32 * wave + qi;
   const int kload = my_key < tile.nk ? my_key : tile.nk - 1;
+  int kpos;
+  {
+    const int u = tile.u0 + my_key;
+    kpos = u < seq.c ? tile.step * seq.c + u : (2 * p.C - 1 - tile.step) * seq.c + (u - seq.c);
+    if (my_key >= tile.nk) kpos = 0x7fffffff;
+  }
+
+  // ---- direct-load rows: lane carries tile rows 32*(w%2) + 16j + lane/4
+  // (j = 0, 1) of Q (wavefronts 0-1) or dO (2-3); wavefronts 0-2 also load
+  // one statistic of row `lane`.  Rows without a token read the tile's first
+  // row (finite data) and the sentinel token's limit -1.
+  const bf16* src = wave >= 2 ? p.gtok : p.qtok;
+  int dtl[2], dhg[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int row = 32 * (wave & 1) + 16 * j + (lane >> 2);
+    dtl[j] = row / G;
+    dhg[j] = row - dtl[j] * G;
+  }
+  const int stl = lane / G, shg = lane - stl * G;
+  auto issue = [&](int t) {
+    QTileLds& b = qs[t % 3];
+    // past the end: the last tile again, into the idle buffer
+    const int qt0 = tile.q_begin + (t < ntiles ? t : ntiles - 1) * tpt;
+    if (wave < 3) {
+      const int tok = qt0 + stl;
+      const bool ok = stl < tpt && tok < tile.q_end;
+      const int64_t r = (int64_t)(ok ? tok : qt0) * p.hq + head0 + (ok ? shg : 0);
+      if (wave == 0) dma4_async(&p.rowstat[r].x, lds_addr(b.l2));
+      else if (wave == 1) dma4_async(&p.rowstat[r].y, lds_addr(b.dl));
+      else dma4_async(&p.toks[ok ? tok : p.num_tokens].P, lds_addr(b.pl));
+    }
+    bf16* dst = wave >= 2 ? b.g : b.q;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int tok = qt0 + dtl[j];
+      const bool ok = dtl[j] < tpt && tok < tile.q_end;
+      const bf16* rp = src + ((int64_t)(ok ? tok : qt0) * p.hq + head0 + (ok ? dhg[j] : 0)) * kHeadDim;
+#pragma unroll
+      for (int pl = 0; pl < 4; ++pl) {
+        const int m = 8 * (wave & 1) + 4 * j + pl;
+        dma16_async(rp + dma_col<kBwdRows>(m, lane), lds_addr(dma_dst<kBwdRows>(dst, m)));
+      }
+    }
+  };
+
   bf16x8 kreg[8], vreg[8];
   {
     const bf16* kp = p.k_step[tile.step] + (key0 + kload) * kv_row_stride + tile.kvh * kHeadDim;
@@ -184,93 +194,106 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
     dk[nt] = f32x16{};
     dv[nt] = f32x16{};
   }
+  issue(0);
+  issue(1);
   __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  lds_barrier();
 
-  // ---- one query tile on LDS buffer B while tile it+1 is fetched into B^1
-  auto step = [&](int it, auto buf_tag) {
-    constexpr int B = decltype(buf_tag)::value;
-    const QTileLds& cur = qs[B];
-    const int qt0 = tile.q_begin + it * tpt;
-    const bool more = it + 1 < ntiles;
-    RowStats nst{0.f, 0.f, 0};
-    if (more) nst = fetch_qtile(p, tile, seq, qt0 + tpt, tid, qs[B ^ 1]);
-    const bool need_mask =
-        qt0 < tile.q_full || qt0 + tpt > tile.q_end || tile.nk < kBwdKeys || tpt * p.G < kBwdRows;
+  // ---- the stage.  MFMA j: j < 32 -> S (even j) / dP (odd j) of row block
+  // j/16, reduction chunk (j/2)%8; j >= 32 -> dV (even) / dK (odd), column
+  // block ((j-32)/2)%4, reduction block t = (j-32)/8 (query rows 16t..16t+15;
+  // a lane of half h holds rows 16t+4h+{0..3} and 16t+8+4h+{0..3}, so the
+  // dO / Q operand is read column-wise from the same rows).
+  // Softmax element e (slot 16+e): accumulator slot e%16 of row block e/16,
+  // query row 32(e/16) + 8((e%16)/4) + 4h + e%4.
+  auto stage = [&](const QTileLds& cur, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    f32x16 s[2], dp[2];
+    bf16x8 opq[kOpAhead + 1];
+    float4 sl[8], sd[8];
+    int4 sp[8];
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    bf16x2 pp[16], pd[16];
+    float prv = 0.f, dsv = 0.f;
 
-    auto body = [&](auto mask_tag) {
-      constexpr bool MASK = decltype(mask_tag)::value;
-      // ---- S = Q K^T, dP = dO V^T (rows = queries, column = this lane's key)
-      f32x16 s[2], dp[2];
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-        s[mt] = f32x16{};
-        dp[mt] = f32x16{};
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          s[mt] = mfma32(ld16(&cur.q[tile_off<kBwdRows>(32 * mt + qi, 16 * c + 8 * half)]), kreg[c], s[mt]);
-          dp[mt] = mfma32(ld16(&cur.g[tile_off<kBwdRows>(32 * mt + qi, 16 * c + 8 * half)]), vreg[c], dp[mt]);
-        }
+    auto load_op = [&](int j) -> bf16x8 {
+      if (j < 32) {
+        const int off = tile_off<kBwdRows>(32 * (j >> 4) + qi, 16 * ((j >> 1) & 7) + 8 * half);
+        return ld16((j & 1) ? &cur.g[off] : &cur.q[off]);
       }
-      // phase fences: reads of a later phase hoisted over this one would
-      // keep their results live across it and exhaust the registers
-      __builtin_amdgcn_sched_barrier(0);
-      // ---- P = exp2(S scale log2e - LSE log2e), dS = P (dP - Delta)
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-        for (int vq = 0; vq < 4; ++vq) {
-          const int r0 = 32 * mt + 8 * vq + 4 * half;
-          const float4 l4 = *reinterpret_cast<const float4*>(&cur.l2[r0]);
-          const float4 d4 = *reinterpret_cast<const float4*>(&cur.dl[r0]);
-          const int4 m4 = *reinterpret_cast<const int4*>(&cur.lim[r0]);
-          const float lr[4] = {l4.x, l4.y, l4.z, l4.w};
-          const float dr[4] = {d4.x, d4.y, d4.z, d4.w};
-          const int mr[4] = {m4.x, m4.y, m4.z, m4.w};
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const int v = 4 * vq + c;
-            float pr = fast_exp2(__builtin_fmaf(s[mt][v], p.scale_log2, -lr[c]));
-            if (MASK && my_key >= mr[c]) pr = 0.f;
-            s[mt][v] = pr;
-            dp[mt][v] = pr * (dp[mt][v] - dr[c]);
-          }
-        }
+      const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3;
+      return ld_tr8<kBwdRows>((jj & 1) ? cur.q : cur.g, 32 * nt, 16 * t + 4 * half, 16 * t + 8 + 4 * half,
+                              lane);
+    };
+    auto load_stats = [&](int q) {
+      const int r0 = 32 * (q >> 2) + 8 * (q & 3) + 4 * half;
+      sl[q] = *reinterpret_cast<const float4*>(&cur.l2[r0]);
+      sd[q] = *reinterpret_cast<const float4*>(&cur.dl[r0]);
+      if (MASK) sp[q] = *reinterpret_cast<const int4*>(&cur.pl[r0]);
+    };
+    auto softmax = [&](int e) {
+      const int mt = e >> 4, v = e & 15, q = e >> 2, c = e & 3;
+      const float l = c == 0 ? sl[q].x : c == 1 ? sl[q].y : c == 2 ? sl[q].z : sl[q].w;
+      const float d = c == 0 ? sd[q].x : c == 1 ? sd[q].y : c == 2 ? sd[q].z : sd[q].w;
+      float pr = fast_exp2(__builtin_fmaf(s[mt][v], p.scale_log2, -l));
+      if (MASK) {
+        const int lim = c == 0 ? sp[q].x : c == 1 ? sp[q].y : c == 2 ? sp[q].z : sp[q].w;
+        pr = kpos <= lim ? pr : 0.f;
       }
-      __builtin_amdgcn_sched_barrier(0);
-      // ---- dV += P^T dO, dK += dS^T Q.  k-block t covers query rows 16t..16t+15;
-      // a lane of half h holds rows 16t+4h+{0..3} and 16t+8+4h+{0..3} of it, so
-      // the dO / Q operand is read column-wise from the same rows.
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int v0 = 8 * (t & 1);
-        const f32x16& ps = s[t >> 1];
-        const f32x16& dss = dp[t >> 1];
-        const bf16x8 pa =
-            pack8(ps[v0], ps[v0 + 1], ps[v0 + 2], ps[v0 + 3], ps[v0 + 4], ps[v0 + 5], ps[v0 + 6], ps[v0 + 7]);
-        const bf16x8 dsa = pack8(dss[v0], dss[v0 + 1], dss[v0 + 2], dss[v0 + 3], dss[v0 + 4], dss[v0 + 5],
-                                 dss[v0 + 6], dss[v0 + 7]);
-        const int ka = 16 * t + 4 * half, kb = ka + 8;
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-          dv[nt] = mfma32(pa, ld_tr8<kBwdRows>(cur.g, 32 * nt, ka, kb, lane), dv[nt]);
-          dk[nt] = mfma32(dsa, ld_tr8<kBwdRows>(cur.q, 32 * nt, ka, kb, lane), dk[nt]);
-        }
+      const float ds = pr * (dp[mt][v] - d);
+      if (e & 1) {
+        pp[e >> 1] = bf16x2{(bf16)prv, (bf16)pr};
+        pd[e >> 1] = bf16x2{(bf16)dsv, (bf16)ds};
+      } else {
+        prv = pr;
+        dsv = ds;
       }
     };
-    if (need_mask) body(std::true_type{});
-    else body(std::false_type{});
+    auto pa = [&](int t) {
+      return bf16x8{pp[4 * t][0], pp[4 * t][1], pp[4 * t + 1][0], pp[4 * t + 1][1],
+                    pp[4 * t + 2][0], pp[4 * t + 2][1], pp[4 * t + 3][0], pp[4 * t + 3][1]};
+    };
+    auto dsa = [&](int t) {
+      return bf16x8{pd[4 * t][0], pd[4 * t][1], pd[4 * t + 1][0], pd[4 * t + 1][1],
+                    pd[4 * t + 2][0], pd[4 * t + 2][1], pd[4 * t + 3][0], pd[4 * t + 3][1]};
+    };
+    auto mfma = [&](int j, const bf16x8& a) {
+      if (j < 32) {
+        const int mt = j >> 4, c = (j >> 1) & 7;
+        if (j & 1) dp[mt] = mfma32(a, vreg[c], c ? dp[mt] : f32x16{});
+        else s[mt] = mfma32(a, kreg[c], c ? s[mt] : f32x16{});
+      } else {
+        const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3;
+        if (jj & 1) dk[nt] = mfma32(dsa(t), a, dk[nt]);
+        else dv[nt] = mfma32(pa(t), a, dv[nt]);
+      }
+    };
 
-    if (more) store_stats(qs[B ^ 1], nst, tid);
-    __builtin_amdgcn_s_waitcnt(0);  // this wavefront's direct loads have landed
-    __syncthreads();
+    static_for<kOpAhead>([&](auto jc) { opq[jc.value] = load_op(jc.value); });
+    static_for<64>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      if constexpr (j + kOpAhead < 64) opq[(j + kOpAhead) % (kOpAhead + 1)] = load_op(j + kOpAhead);
+      if constexpr (j >= 12 && j < 44 && (j & 3) == 0) load_stats((j - 12) >> 2);
+      if constexpr (j >= 16 && j < 48) softmax(j - 16);
+      mfma(j, opq[j % (kOpAhead + 1)]);
+      __builtin_amdgcn_sched_barrier(0);
+    });
   };
-  int it = 0;
-  for (; it + 1 < ntiles; it += 2) {
-    step(it, std::integral_constant<int, 0>{});
-    step(it + 1, std::integral_constant<int, 1>{});
+
+  for (int it = 0; it < ntiles; ++it) {
+    issue(it + 2);
+    const QTileLds& cur = qs[it % 3];
+    const int qt0 = tile.q_begin + it * tpt;
+    const bool need_mask =
+        qt0 < tile.q_full || qt0 + tpt > tile.q_end || tile.nk < kBwdKeys || tpt * G < kBwdRows;
+    if (need_mask) stage(cur, std::true_type{});
+    else stage(cur, std::false_type{});
+    // tile it+1 (issued one stage ago) has landed for this wavefront; the
+    // loads of tile it+2 stay in flight
+    wait_vmcnt_lgkm0<kDmaPerStage>();
+    lds_barrier();
   }
-  if (it < ntiles) step(it, std::integral_constant<int, 0>{});
+  __builtin_amdgcn_s_waitcnt(0);  // no direct load outlives the workgroup
 
   // ---- write dK (scaled) and dV: accumulator column = dim, rows = keys
   void* dkout = p.dk_step[tile.step];

@@ -12,6 +12,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace ba {
 
 typedef __bf16 bf16;
@@ -105,6 +108,63 @@ __device__ __forceinline__ int dma_col(int m, int lane) {
 template <int R>
 __device__ __forceinline__ bf16* dma_dst(bf16* T, int m) {
   return T + (((m & 3) * R + 16 * (m >> 2)) << 5);
+}
+
+// The same copies issued as inline assembly, invisible to the compiler's
+// wait-count tracking.  The builtin above makes the compiler wait for every
+// outstanding direct load before any LDS read it cannot prove disjoint,
+// which serialises a prefetch pipeline; with these the caller waits on the
+// vector-memory counter itself (wait_vmcnt) before the data is read, and no
+// compiler-visible vector-memory load may be outstanding where such a wait
+// matters.  m0 carries the LDS base; lds_addr must be wavefront-uniform.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16_async(const void* src, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_addr) : "memory", "m0");
+}
+__device__ __forceinline__ void dma4_async(const void* src, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(lds_addr) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// 32-bit LDS address of a shared-memory pointer, as a wavefront-uniform value
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)(p));
+}
+
+// s_waitcnt vmcnt(N) (expcnt and lgkmcnt left alone) / vmcnt(N) lgkmcnt(0)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+// Workgroup barrier that, unlike __syncthreads, does not drain the vector
+// memory counter; the caller has already waited for what the other
+// wavefronts will read.  The empty asm statements keep the compiler from
+// moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Compile-time loop: f(std::integral_constant<int, i>) for i = 0 .. N-1, so
+// that every index inside the body is a constant even where a large body
+// would exceed the unroller's limits.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

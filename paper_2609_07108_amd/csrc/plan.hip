@@ -57,6 +57,10 @@ WorkspaceLayout workspace_layout(const Plan& p, int mode) {
   off = after_tables;
   w.rowstat = off;
   off = align(off + rows * 2 * sizeof(float));
+  w.qtok = off;
+  off = align(off + rows * kHeadDim * sizeof(uint16_t));
+  w.gtok = off;
+  off = align(off + rows * kHeadDim * sizeof(uint16_t));
   if (mode == BA_MODE_PER_STEP) {
     w.dq_acc = off;
     off = align(off + rows * kHeadDim * sizeof(float));
@@ -241,7 +245,11 @@ static int build_plan(const ba_problem* pr, Plan& P) {
   // --- packed table image
   P.image.clear();
   P.off_seqs = append(P.image, P.seqs);
-  P.off_toks = append(P.image, P.toks);
+  // the token table is followed by a sentinel whose causal limit -1 admits
+  // no key: kernels point rows without a token at it
+  std::vector<TokInfo> toks_img(P.toks);
+  toks_img.push_back(TokInfo{0, -1, -1, 0});
+  P.off_toks = append(P.image, toks_img);
   P.off_groups = append(P.image, P.groups);
   P.off_fwd = append(P.image, P.fwd_tiles);
   P.off_bwd = append(P.image, P.bwd_tiles);
