@@ -117,7 +117,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   const SeqInfo seq = p.seqs[tile.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform
   const int qi = lane & 31;
   const int half = lane >> 5;
   const int G = p.G;
@@ -152,28 +152,36 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
     dhg[j] = row - dtl[j] * G;
   }
   const int stl = lane / G, shg = lane - stl * G;
+  const uint32_t qs_lds = lds_addr(&qs[0]);
   auto issue = [&](int t) {
-    QTileLds& b = qs[t % 3];
+    const uint32_t b = qs_lds + (uint32_t)(t % 3) * (uint32_t)sizeof(QTileLds);
     // past the end: the last tile again, into the idle buffer
     const int qt0 = tile.q_begin + (t < ntiles ? t : ntiles - 1) * tpt;
+    const int nt = tile.q_end - qt0;  // tokens left from qt0
     if (wave < 3) {
-      const int tok = qt0 + stl;
-      const bool ok = stl < tpt && tok < tile.q_end;
-      const int64_t r = (int64_t)(ok ? tok : qt0) * p.hq + head0 + (ok ? shg : 0);
-      if (wave == 0) dma4_async(&p.rowstat[r].x, lds_addr(b.l2));
-      else if (wave == 1) dma4_async(&p.rowstat[r].y, lds_addr(b.dl));
-      else dma4_async(&p.toks[ok ? tok : p.num_tokens].P, lds_addr(b.pl));
+      const bool ok = stl < tpt && stl < nt;
+      if (wave == 2) {
+        const void* base = uniform_ptr(p.toks + qt0);
+        const uint32_t off = (uint32_t)((ok ? stl : p.num_tokens - qt0) * (int)sizeof(TokInfo) +
+                                        (int)offsetof(TokInfo, P));
+        dma4_async(base, off, b + (uint32_t)offsetof(QTileLds, pl));
+      } else {
+        const void* base = uniform_ptr(p.rowstat + (int64_t)qt0 * p.hq + head0);
+        const uint32_t off = (uint32_t)((ok ? stl * p.hq + shg : 0) * (int)sizeof(float2) + 4 * wave);
+        dma4_async(base, off, b + (uint32_t)(wave == 0 ? offsetof(QTileLds, l2) : offsetof(QTileLds, dl)));
+      }
     }
-    bf16* dst = wave >= 2 ? b.g : b.q;
+    const uint32_t dst = b + (uint32_t)(wave >= 2 ? offsetof(QTileLds, g) : offsetof(QTileLds, q));
+    const void* base = uniform_ptr(src + ((int64_t)qt0 * p.hq + head0) * kHeadDim);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int tok = qt0 + dtl[j];
-      const bool ok = dtl[j] < tpt && tok < tile.q_end;
-      const bf16* rp = src + ((int64_t)(ok ? tok : qt0) * p.hq + head0 + (ok ? dhg[j] : 0)) * kHeadDim;
+      const bool ok = dtl[j] < tpt && dtl[j] < nt;
+      const int r = ok ? dtl[j] * p.hq + dhg[j] : 0;  // row relative to (qt0, head0)
 #pragma unroll
       for (int pl = 0; pl < 4; ++pl) {
         const int m = 8 * (wave & 1) + 4 * j + pl;
-        dma16_async(rp + dma_col<kBwdRows>(m, lane), lds_addr(dma_dst<kBwdRows>(dst, m)));
+        const uint32_t off = (uint32_t)(r * kHeadDim + dma_col<kBwdRows>(m, lane)) * (uint32_t)sizeof(bf16);
+        dma16_async(base, off, dst + dma_dst_bytes<kBwdRows>(m));
       }
     }
   };
@@ -324,7 +332,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
   const SeqInfo seq = p.seqs[tile.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform
   const int qi = lane & 31;
   const int half = lane >> 5;
   const int row = wave * 32 + qi;

@@ -109,25 +109,45 @@ template <int R>
 __device__ __forceinline__ bf16* dma_dst(bf16* T, int m) {
   return T + (((m & 3) * R + 16 * (m >> 2)) << 5);
 }
+// the same destination as a byte offset from the tile's start
+template <int R>
+__device__ __forceinline__ constexpr uint32_t dma_dst_bytes(int m) {
+  return (uint32_t)((((m & 3) * R + 16 * (m >> 2)) << 5) * 2);
+}
 
 // The same copies issued as inline assembly, invisible to the compiler's
 // wait-count tracking.  The builtin above makes the compiler wait for every
 // outstanding direct load before any LDS read it cannot prove disjoint,
 // which serialises a prefetch pipeline; with these the caller waits on the
-// vector-memory counter itself (wait_vmcnt) before the data is read, and no
-// compiler-visible vector-memory load may be outstanding where such a wait
-// matters.  m0 carries the LDS base; lds_addr must be wavefront-uniform.
+// vector-memory counter itself (wait_vmcnt) before the data is read.  Any
+// compiler-visible vector-memory access (a global load, a register spill)
+// issued while such loads are in flight makes the compiler's own waits
+// cover them too, so loops that use these must be free of both.
+// The address is a wavefront-uniform base plus a 32-bit per-lane byte
+// offset; m0 carries the LDS base, also wavefront-uniform.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16_async(const void* src, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_addr) : "memory", "m0");
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
 }
-__device__ __forceinline__ void dma4_async(const void* src, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(lds_addr) : "memory", "m0");
+__device__ __forceinline__ void dma16_async(const void* base, uint32_t off, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base),
+               "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma4_async(const void* base, uint32_t off, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(off), "s"(base),
+               "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+               : "memory", "m0");
 }
 #pragma clang diagnostic pop
 
-// 32-bit LDS address of a shared-memory pointer, as a wavefront-uniform value
+// 32-bit LDS address of a shared-memory pointer, as a wavefront-uniform
+// value.  Take it once per kernel and add byte offsets: converting generic
+// pointers inside a loop costs a null check and 64-bit registers.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)(p));

@@ -53,7 +53,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const SeqInfo seq = p.seqs[tile.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform
   const int qi = lane & 31;
   const int half = lane >> 5;
   const int row = wave * 32 + qi;

@@ -84,7 +84,10 @@ struct BwdParams {
 // can see.  Each tile's K and V rows are fetched with direct global-to-LDS
 // loads into plane tiles (see tile_off), double-buffered: while `body`
 // computes on one buffer the next tile, possibly of the next ring step, is
-// already in flight into the other.  The buffers are used in a fixed
+// already in flight into the other.  The loads are not tracked by the
+// compiler (dma16_async), so the body's LDS reads do not wait for them; the
+// walk waits explicitly before each barrier, and the body issues no global
+// loads of its own.  The buffers are used in a fixed
 // alternation so their LDS addresses are compile-time constants in the body.
 // body(j, kv0, ks, vs) is called once per tile with the ring block j, the
 // first key kv0 (index inside the sequence's segment of block j) and the
@@ -112,37 +115,43 @@ __device__ __forceinline__ void walk_kv_tiles(const P& p, const SeqInfo& seq, in
     c.kv0 += kFwdKeys;
     return c.kv0 < c.lim_hi ? c : seek(c.i + 1);
   };
-  auto fetch = [&](const KvCursor& c, bf16* kd, bf16* vd) {
-    const bf16* kb = p.k_step[c.j] + (int64_t)seq.seg_off * stride + kvh * kHeadDim;
-    const bf16* vb = p.v_step[c.j] + (int64_t)seq.seg_off * stride + kvh * kHeadDim;
+  constexpr uint32_t kTileBytes = kFwdKeys * kHeadDim * sizeof(bf16);
+  const uint32_t kv_lds = lds_addr(&kv[0][0][0]);  // [buffer][K, V] tiles follow each other
+  auto fetch = [&](const KvCursor& c, int buf) {
+    const uint32_t kd = kv_lds + (2 * buf) * kTileBytes, vd = kd + kTileBytes;
+    // base: the tile's first key row (uniform); per lane a byte offset
+    const int64_t row0 = ((int64_t)seq.seg_off + c.kv0) * stride + kvh * kHeadDim;
+    const void* kb = uniform_ptr(p.k_step[c.j] + row0);
+    const void* vb = uniform_ptr(p.v_step[c.j] + row0);
+    const int nrow = c.lim_hi - c.kv0;  // rows past the visible prefix repeat its last row
 #pragma unroll
     for (int m4 = 0; m4 < 4; ++m4) {
       const int m = 4 * wave + m4;  // 16 loads per tensor and tile, 4 per wavefront
-      int u = c.kv0 + dma_row<kFwdKeys>(m, lane);
-      u = u < c.lim_hi ? u : c.lim_hi - 1;
-      const int col = dma_col<kFwdKeys>(m, lane);
-      dma16(kb + (int64_t)u * stride + col, dma_dst<kFwdKeys>(kd, m));
-      dma16(vb + (int64_t)u * stride + col, dma_dst<kFwdKeys>(vd, m));
+      int u = dma_row<kFwdKeys>(m, lane);
+      u = u < nrow ? u : nrow - 1;
+      const uint32_t off = (uint32_t)(u * (int)stride + dma_col<kFwdKeys>(m, lane)) * (uint32_t)sizeof(bf16);
+      dma16_async(kb, off, kd + dma_dst_bytes<kFwdKeys>(m));
+      dma16_async(vb, off, vd + dma_dst_bytes<kFwdKeys>(m));
     }
   };
   KvCursor cur = seek(p.step_first);
   if (cur.i >= step_end) return;
-  fetch(cur, kv[0][0], kv[0][1]);
+  fetch(cur, 0);
   __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  lds_barrier();
   while (true) {
     KvCursor nx = next(cur);
-    if (nx.i < step_end) fetch(nx, kv[1][0], kv[1][1]);
+    if (nx.i < step_end) fetch(nx, 1);
     body(cur.j, cur.kv0, kv[0][0], kv[0][1]);
-    __builtin_amdgcn_s_waitcnt(0);  // this wavefront's loads of the next tile have landed
-    __syncthreads();
+    wait_vmcnt_lgkm0<0>();  // this wavefront's loads of the next tile have landed
+    lds_barrier();
     if (nx.i >= step_end) return;
     cur = nx;
     nx = next(cur);
-    if (nx.i < step_end) fetch(nx, kv[0][0], kv[0][1]);
+    if (nx.i < step_end) fetch(nx, 0);
     body(cur.j, cur.kv0, kv[1][0], kv[1][1]);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    wait_vmcnt_lgkm0<0>();
+    lds_barrier();
     if (nx.i >= step_end) return;
     cur = nx;
   }
