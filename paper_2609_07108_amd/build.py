@@ -26,8 +26,13 @@ HOST_SOURCES = []
 ARCH = "gfx950"
 COMMON_FLAGS = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
                 f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
+# -amdgpu-mfma-vgpr-form: MFMA results go to ordinary vector registers.  The
+# dK/dV kernel runs one wavefront per SIMD (512 registers) and would
+# otherwise get every MFMA accumulator in the accumulation registers, with a
+# copy per softmax element; its long-lived dK/dV accumulators are pinned to
+# the accumulation registers explicitly instead.
 HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-             "-munsafe-fp-atomics"]
+             "-munsafe-fp-atomics", "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
 def hipcc() -> str:

@@ -199,8 +199,8 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   f32x16 dk[4], dv[4];
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) {
-    dk[nt] = f32x16{};
-    dv[nt] = f32x16{};
+    mfma32_acc_zero(dk[nt]);
+    mfma32_acc_zero(dv[nt]);
   }
   issue(0);
   issue(1);
@@ -272,8 +272,8 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
         else s[mt] = mfma32(a, kreg[c], c ? s[mt] : f32x16{});
       } else {
         const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3;
-        if (jj & 1) dk[nt] = mfma32(dsa(t), a, dk[nt]);
-        else dv[nt] = mfma32(pa(t), a, dv[nt]);
+        if (jj & 1) mfma32_acc(dk[nt], dsa(t), a);
+        else mfma32_acc(dv[nt], pa(t), a);
       }
     };
 
@@ -288,19 +288,29 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
     });
   };
 
-  for (int it = 0; it < ntiles; ++it) {
-    issue(it + 2);
-    const QTileLds& cur = qs[it % 3];
-    const int qt0 = tile.q_begin + it * tpt;
-    const bool need_mask =
-        qt0 < tile.q_full || qt0 + tpt > tile.q_end || tile.nk < kBwdKeys || tpt * G < kBwdRows;
-    if (need_mask) stage(cur, std::true_type{});
-    else stage(cur, std::false_type{});
-    // tile it+1 (issued one stage ago) has landed for this wavefront; the
-    // loads of tile it+2 stay in flight
-    wait_vmcnt_lgkm0<kDmaPerStage>();
-    lds_barrier();
+  // Tiles [t_lo, t_hi) need no mask: every row has a token and sees all
+  // keys of the block (tokens from q_full on do).  The three ranges run as
+  // separate loops so each has one stage variant and the accumulators stay
+  // in place across iterations.
+  int t_lo = ntiles, t_hi = ntiles;
+  if (tile.nk == kBwdKeys && tpt * G == kBwdRows) {
+    t_lo = min(ntiles, max(0, (tile.q_full - tile.q_begin + tpt - 1) / tpt));
+    t_hi = max(t_lo, (tile.q_end - tile.q_begin) / tpt);
   }
+  auto run = [&](int t0, int t1, auto mask_tag) {
+    for (int it = t0; it < t1; ++it) {
+      issue(it + 2);
+      stage(qs[it % 3], mask_tag);
+      // tile it+1 (issued one stage ago) has landed for this wavefront; the
+      // loads of tile it+2 stay in flight
+      wait_vmcnt_lgkm0<kDmaPerStage>();
+      lds_barrier();
+    }
+    mfma_drain();  // accumulators settled before the compiler may move them
+  };
+  run(0, t_lo, std::true_type{});
+  run(t_lo, t_hi, std::false_type{});
+  run(t_hi, ntiles, std::true_type{});
   __builtin_amdgcn_s_waitcnt(0);  // no direct load outlives the workgroup
 
   // ---- write dK (scaled) and dV: accumulator column = dim, rows = keys

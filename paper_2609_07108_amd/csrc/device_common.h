@@ -27,6 +27,27 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// The same MFMA with its accumulator pinned to the accumulation registers
+// (AGPRs), for long-lived accumulators that only MFMAs touch: the compiler
+// then keeps them there instead of moving them between register files.  It
+// does not see this as an MFMA, so the caller guarantees the hazards it
+// would otherwise pad: the A/B operands are not written by a VALU
+// instruction just before (two wait states are padded), no other MFMA
+// writes the accumulator within the latency of this one, and mfma_drain()
+// separates the last one from any VALU read or move of the accumulator.
+__device__ __forceinline__ void mfma32_acc(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  // s_nop 1: two wait states for an operand just written by a VALU instruction
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// A zero accumulator produced in the accumulation registers (an MFMA of zero
+// operands with a zero addend), so a loop-carried accumulator never has a
+// definition outside them.
+__device__ __forceinline__ void mfma32_acc_zero(f32x16& acc) {
+  const bf16x8 z = bf16x8{};
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %1, 0" : "=a"(acc) : "v"(z));
+}
+__device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory"); }
+
 __device__ __forceinline__ bf16x8 ld16(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 __device__ __forceinline__ void st16(bf16* p, const bf16x8& v) { *reinterpret_cast<bf16x8*>(p) = v; }
 
