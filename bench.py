@@ -37,11 +37,10 @@ PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/c
 # calibration (profiles/traffic_eagle3-K3-L262144-cp8r0.md).  A figure only
 # applies while the kernel's source is the one that was measured.
 MEASURED_TRAFFIC = {
-    ("bwd_kv_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "e495667509d65906", "bytes": 189371247257},
-    ("bwd_dq_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "e495667509d65906", "bytes": 1879061264353},
-    ("fwd_kernel", "fused"): {"source": "fwd.hip", "sha256_16": "d22e737329a6928d", "bytes": 688617242893},
+    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "e63980113a06671f", "bytes": 34734704529},
+    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "e63980113a06671f", "bytes": 14991758760},
+    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "fed3ba8aec22a72b", "bytes": 14552419957},
 }
-
 
 def measured_traffic(kernel: str, workload: str, mode: str):
     """HBM bytes per launch of `kernel`, or None if not measured for this
@@ -249,7 +248,8 @@ def main():
                      "peak": round(PEAK_BF16_TFLOPS, 1), "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic,
-                     "launches_per_step": launches},
+                     "launches_per_step": launches,
+                     "launch_ms": round(dom_ms / launches, 3)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
