@@ -28,7 +28,7 @@ namespace ba {
 
 // tile shapes (the kernels are written for exactly these)
 constexpr int kHeadDim = 128;
-constexpr int kFwdRows = 128;   // query rows (token x head) per forward tile
+constexpr int kFwdRows = 256;   // query rows (token x head) per forward tile
 constexpr int kFwdKeys = 64;    // keys per forward inner iteration
 constexpr int kBwdKeys = 128;   // keys owned by one backward work item
 constexpr int kBwdRows = 64;    // query rows per backward inner iteration

@@ -312,6 +312,11 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   run(t_lo, t_hi, std::false_type{});
   run(t_hi, ntiles, std::true_type{});
   __builtin_amdgcn_s_waitcnt(0);  // no direct load outlives the workgroup
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt) {  // the reads below stay after the last drain
+    acc_settle(dk[nt]);
+    acc_settle(dv[nt]);
+  }
 
   // ---- write dK (scaled) and dV: accumulator column = dim, rows = keys
   void* dkout = p.dk_step[tile.step];
@@ -330,7 +335,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------ dq
-// Query tile of 128 rows (4 wavefronts x 32), the same tiles as the forward.
+// Half a forward query tile, 128 rows (4 wavefronts x 32), per workgroup.
 // Accumulator layout: dQ^T, lane = one query row, rows = dims
 // 32*dt + 8*(v/4) + 4*half + v%4.
 template <int MODE>
@@ -338,14 +343,17 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
   // [buffer][K, V] plane tiles of 64 keys (see tile_off), double-buffered
   __shared__ __attribute__((aligned(16))) bf16 kvbuf[2][2][kFwdKeys * kHeadDim];
 
-  const FwdTile tile = p.qtiles[blockIdx.x];
+  // two workgroups per query tile: rows [128 h, 128 h + 128) of it
+  const FwdTile tile = p.qtiles[blockIdx.x >> 1];
+  const int rbase = 128 * (blockIdx.x & 1);
+  if (rbase / p.G >= tile.ntok) return;  // no token in this half
   const SeqInfo seq = p.seqs[tile.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform
   const int qi = lane & 31;
   const int half = lane >> 5;
-  const int row = wave * 32 + qi;
+  const int row = rbase + wave * 32 + qi;
   const int tl = row / p.G;
   const int head = tile.kvh * p.G + (row - tl * p.G);
   const bool valid = tl < tile.ntok;
@@ -379,8 +387,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) dq[dt] = f32x16{};
 
-  const int Pmin = p.toks[tile.tok_begin].P;
-  const int Pmax = p.toks[tile.tok_begin + tile.ntok - 1].P;
+  const int Pmin = p.toks[tile.tok_begin + rbase / p.G].P;
+  const int Pmax = p.toks[tile.tok_begin + min(tile.ntok - 1, (rbase + 127) / p.G)].P;
   const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
 
   if (MODE != kModeFinal) {
@@ -600,7 +608,7 @@ hipError_t launch_bwd_kv(const BwdParams& p, hipStream_t stream) {
 
 hipError_t launch_bwd_dq(const BwdParams& p, int mode, hipStream_t stream) {
   if (p.num_qtiles == 0) return hipSuccess;
-  dim3 grid(p.num_qtiles), block(256);
+  dim3 grid(2 * p.num_qtiles), block(256);
   if (mode == kModeStep) hipLaunchKernelGGL(bwd_dq_kernel<kModeStep>, grid, block, 0, stream, p);
   else if (mode == kModeFinal) hipLaunchKernelGGL(bwd_dq_kernel<kModeFinal>, grid, block, 0, stream, p);
   else hipLaunchKernelGGL(bwd_dq_kernel<kModeFused>, grid, block, 0, stream, p);

@@ -39,6 +39,25 @@ __device__ __forceinline__ void mfma32_acc(f32x16& acc, const bf16x8& a, const b
   // s_nop 1: two wait states for an operand just written by a VALU instruction
   asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
+// MFMA with a vector-register accumulator and the B operand held in the
+// accumulation registers (so long-lived B operands do not occupy vector
+// registers).  Opaque to the hazard recognizer: the caller keeps the result
+// away from vector-ALU reads until the MFMA has completed (mfma_drain, or
+// enough later instructions) and does not write the A operand just before.
+__device__ __forceinline__ void mfma32_v_first(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(a), "a"(b));
+}
+__device__ __forceinline__ void mfma32_v(f32x16& d, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "a"(b));
+}
+
+// 16-byte global load straight into accumulation registers (for MFMA
+// operands that stay resident there).  Untracked by the compiler: the caller
+// waits on the vector-memory counter before the first use.
+__device__ __forceinline__ void load16_agpr(bf16x8& d, const bf16* src) {
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=a"(d) : "v"(src) : "memory");
+}
+
 // A zero accumulator produced in the accumulation registers (an MFMA of zero
 // operands with a zero addend), so a loop-carried accumulator never has a
 // definition outside them.
@@ -46,6 +65,23 @@ __device__ __forceinline__ void mfma32_acc_zero(f32x16& acc) {
   const bf16x8 z = bf16x8{};
   asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %1, 0" : "=a"(acc) : "v"(z));
 }
+// Rescale an accumulator held in the accumulation registers by a per-lane
+// factor.  Empty asm statements with accumulation-register operands bracket
+// the vector-ALU multiply, so the accumulator keeps a single register class
+// and the compiler neither hoists the reads nor copies it elsewhere.  Call
+// between two mfma_drain().
+__device__ __forceinline__ void acc_scale(f32x16& acc, float alpha) {
+  asm volatile("" : "+a"(acc));  // the reads below stay here, not hoisted
+  const f32x16 t = acc * alpha;
+  asm volatile("" : "=a"(acc) : "0"(t));
+}
+// Marks an accumulation-register value as redefined here: vector-ALU uses
+// after this point cannot be moved (or copied out) before it.  Place after
+// mfma_drain().
+__device__ __forceinline__ void acc_settle(f32x16& acc) { asm volatile("" : "+a"(acc)); }
+// The same for a vector-register MFMA result of mfma32_v: reads after it
+// cannot be hoisted above a preceding mfma_drain().
+__device__ __forceinline__ void vacc_settle(f32x16& acc) { asm volatile("" : "+v"(acc)); }
 __device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory"); }
 
 __device__ __forceinline__ bf16x8 ld16(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }

@@ -1,9 +1,11 @@
 // Forward branch attention for one context-parallel rank share (Sec. 3.2).
 //
-// One workgroup (4 wavefronts) owns a query tile of 128 rows: up to 128/G
-// query tokens times the G query heads that share one KV head.  Each
-// wavefront holds 32 rows.  Per ring step j the tile walks the visible prefix
-// of rank j's KV block in 64-key tiles:
+// One workgroup (4 wavefronts, one per SIMD) owns a query tile of 256 rows:
+// up to 256/G query tokens times the G query heads that share one KV head.
+// Wavefront w holds rows 64w..64w+63 as two 32-row blocks, so every K and V
+// fragment it reads from LDS feeds two MFMAs (one per row block).  Per ring
+// step j the tile walks the visible prefix of rank j's KV block in 64-key
+// tiles:
 //   S^T = K Q^T       (bf16 MFMA 32x32x16, lane = one query row, so the row
 //                      maximum is an in-register reduction plus one exchange
 //                      with the other half-wavefront)
@@ -11,11 +13,18 @@
 //   O^T += V^T P^T    (P^T taken straight from the S^T accumulator registers;
 //                      V^T read column-wise from the row-major V tile with
 //                      transposing LDS reads, in the matching key order)
-// Tiles that are fully visible to every row skip the mask; the causal limit
-// of a row in block j is a prefix of the block because positions increase
-// with the local index (chunk j, then chunk 2C-1-j).  K and V tiles arrive by
-// direct global-to-LDS loads, double-buffered across ring steps
-// (walk_kv_tiles), so the next tile is in flight during the MFMAs.
+// The tiles are software-pipelined: while the softmax of tile t runs on the
+// vector ALUs, the MFMAs compute S^T of tile t+1 and then O^T += V^T P^T of
+// tile t.  K/V tiles arrive by direct global-to-LDS loads into three
+// buffers (tile t+2 in flight).  O^T and Q^T live in the accumulation
+// registers.  The running maximum used for the exponentials is only moved
+// (and O and the row sum rescaled) when a row's maximum grows by more than
+// kRescaleSlack in log2 units, so probabilities stay below 2^kRescaleSlack;
+// O / l is unchanged by the choice of that reference, so the result is the
+// same up to rounding.  Tiles that are fully visible to every row skip the
+// mask; the causal limit of a row in block j is a prefix of the block
+// because positions increase with the local index (chunk j, then chunk
+// 2C-1-j).
 //
 // Epilogues
 //   STEP  : merge the step's partial (O, LSE) into the running fp32 pair in
@@ -36,18 +45,16 @@ namespace ba {
 
 namespace {
 
-struct RowState {
-  f32x16 o[4];  // O^T accumulator, d = 32*dt + 8*(v/4) + 4*half + v%4
-  float m;      // running max (log2 domain)
-  float l;      // running sum (this lane's keys only until the end)
-};
+constexpr float kRescaleSlack = 8.f;  // log2 of the largest probability before a rescale
+constexpr int kFragAhead = 2;         // LDS operand fragments read ahead of their MFMAs
+constexpr int kKvBufs = 3;
 
 }  // namespace
 
 template <int MODE>
-__global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
-  // [buffer][K, V] plane tiles of 64 keys (see tile_off), double-buffered
-  __shared__ __attribute__((aligned(16))) bf16 kvbuf[2][2][kFwdKeys * kHeadDim];
+__global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
+  // [buffer][K, V] plane tiles of 64 keys (see tile_off)
+  __shared__ __attribute__((aligned(16))) bf16 kvbuf[kKvBufs][2][kFwdKeys * kHeadDim];
 
   const FwdTile tile = p.tiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
@@ -56,260 +63,414 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform
   const int qi = lane & 31;
   const int half = lane >> 5;
-  const int row = wave * 32 + qi;
-  const int tl = row / p.G;
-  const int head = tile.kvh * p.G + (row - tl * p.G);
-  const bool valid = tl < tile.ntok;
-  TokInfo tk;
-  if (valid) tk = p.toks[tile.tok_begin + tl];
-  else tk = TokInfo{0, -1, -1, -1};
+  const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
 
-  const bf16* qptr = tk.qrow >= 0 ? p.q_main + ((int64_t)tk.qrow * p.hq + head) * kHeadDim
-                                  : p.q_br + ((int64_t)(-tk.qrow - 1) * p.hq + head) * kHeadDim;
-  bf16x8 qreg[8];
+  // ---- the lane's two rows (row block rb: row 64 w + 32 rb + qi)
+  int head[2];
+  bool valid[2];
+  TokInfo tk[2];
+  // B operand of S^T = K Q^T (Q^T: k = head dims, n = rows), resident in the
+  // accumulation registers; rows without a token load a row of the tile's
+  // last token (finite, and their results are never written)
+  bf16x8 qreg[2][8];
 #pragma unroll
-  for (int ks8 = 0; ks8 < 8; ++ks8) {
-    if (valid) qreg[ks8] = ld16(qptr + 16 * ks8 + 8 * half);
-    else qreg[ks8] = bf16x8{};
+  for (int rb = 0; rb < 2; ++rb) {
+    const int row = 64 * wave + 32 * rb + qi;
+    const int tl = row / p.G;
+    head[rb] = tile.kvh * p.G + (row - tl * p.G);
+    valid[rb] = tl < tile.ntok;
+    tk[rb] = valid[rb] ? p.toks[tile.tok_begin + tl] : TokInfo{0, -1, -1, -1};
+    const TokInfo tq = valid[rb] ? tk[rb] : p.toks[tile.tok_begin + tile.ntok - 1];
+    const int hq_row = valid[rb] ? head[rb] : tile.kvh * p.G;
+    const bf16* qptr = tq.qrow >= 0 ? p.q_main + ((int64_t)tq.qrow * p.hq + hq_row) * kHeadDim
+                                    : p.q_br + ((int64_t)(-tq.qrow - 1) * p.hq + hq_row) * kHeadDim;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) load16_agpr(qreg[rb][c], qptr + 16 * c + 8 * half);
   }
+  __builtin_amdgcn_s_waitcnt(0);
 
-  RowState st;
+  f32x16 o[2][4];  // O^T accumulators, d = 32 dt + 8 (v/4) + 4 half + v%4
+  float m_use[2] = {-INFINITY, -INFINITY};  // reference maximum of the exponentials (log2)
+  float lsum[2] = {0.f, 0.f};               // this lane's share of the row sum
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt) st.o[dt] = f32x16{};
-  st.m = -INFINITY;
-  st.l = 0.f;
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(o[rb][dt]);
 
   const int Pmin = p.toks[tile.tok_begin].P;
   const int Pmax = p.toks[tile.tok_begin + tile.ntok - 1].P;
-  const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
 
   if (MODE != kModeFinal) {
-    // One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.  MASK
-    // (compile time) only on tiles crossing some row's causal limit.
-    auto compute = [&](int j, int kv0, const bf16* ks, const bf16* vs, auto mask_tag) {
-      constexpr bool MASK = decltype(mask_tag)::value;
-      const int my_lim = valid ? visible_keys(tk.P, j, p.C, seq.c) : 0;
-      // ---- S^T = K Q^T : two 32-key sub-tiles
-      f32x16 s[2];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        s[kt] = f32x16{};
-#pragma unroll
-        for (int ks8 = 0; ks8 < 8; ++ks8)
-          s[kt] = mfma32(ld16(&ks[tile_off<kFwdKeys>(32 * kt + qi, 16 * ks8 + 8 * half)]), qreg[ks8], s[kt]);
+    // ---- cursor over (ring step, 64-key tile): ring step i brings block
+    // j = (rank - i) mod C; tiles cover the prefix of the block that the
+    // tile's largest causal limit can see
+    const int step_end = p.step_first + p.step_count;
+    auto seek = [&](int i) {
+      KvCursor c{i, 0, 0, 0};
+      for (; c.i < step_end; ++c.i) {
+        c.j = ((p.rank - c.i) % p.C + p.C) % p.C;
+        c.lim_hi = visible_keys(Pmax, c.j, p.C, seq.c);
+        if (c.lim_hi > 0) break;
       }
-      // ---- online softmax in the log2 domain; the scale is positive, so
-      // the row maximum is taken on raw scores and applied once
-      float mx = -INFINITY;
+      return c;
+    };
+    auto next = [&](KvCursor c) {
+      if (c.i >= step_end) return c;
+      c.kv0 += kFwdKeys;
+      return c.kv0 < c.lim_hi ? c : seek(c.i + 1);
+    };
+    constexpr uint32_t kTileBytes = kFwdKeys * kHeadDim * sizeof(bf16);
+    const uint32_t kv_lds = lds_addr(&kvbuf[0][0][0]);
+    auto fetch = [&](const KvCursor& c, int buf) {  // direct loads of tile c into buffer buf
+      const int64_t row0 = ((int64_t)seq.seg_off + c.kv0) * kv_row_stride + tile.kvh * kHeadDim;
+      const void* kb = uniform_ptr(p.k_step[c.j] + row0);
+      const void* vb = uniform_ptr(p.v_step[c.j] + row0);
+      const uint32_t kd = kv_lds + (uint32_t)(2 * buf) * kTileBytes, vd = kd + kTileBytes;
+      const int nrow = c.lim_hi - c.kv0;  // rows past the visible prefix repeat its last row
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          if (MASK) {
-            const int u = kv0 + 32 * kt + 8 * (v >> 2) + 4 * half + (v & 3);
-            s[kt][v] = u < my_lim ? s[kt][v] : -INFINITY;
-          }
-          mx = fmaxf(mx, s[kt][v]);
-        }
-      }
-      mx = fmaxf(mx, xor32(mx)) * p.scale_log2;
-      const float m_new = fmaxf(st.m, mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = fast_exp2(st.m - m_use);
-      float lsum = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float e = fast_exp2(__builtin_fmaf(s[kt][v], p.scale_log2, -m_use));
-          s[kt][v] = e;
-          lsum += e;
-        }
-      }
-      st.l = st.l * alpha + lsum;
-      st.m = m_new;
-      // the running output only needs rescaling when some row's maximum grew
-      if (__ballot(alpha != 1.f)) {
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) st.o[dt] *= alpha;
-      }
-      // ---- O^T += V^T P^T : k-block t = keys 16t.. of the tile; a lane of
-      // half h holds keys 16t+4h+{0..3} and 16t+8+4h+{0..3} of it in its S^T
-      // registers, and reads the V^T operand from exactly those key rows
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const f32x16& src = s[t >> 1];
-        const int v0 = 8 * (t & 1);
-        const bf16x8 pb = pack8(src[v0], src[v0 + 1], src[v0 + 2], src[v0 + 3], src[v0 + 4], src[v0 + 5],
-                                src[v0 + 6], src[v0 + 7]);
-        const int ka = 16 * t + 4 * half, kb = ka + 8;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
-          st.o[dt] = mfma32(ld_tr8<kFwdKeys>(vs, 32 * dt, ka, kb, lane), pb, st.o[dt]);
+      for (int m4 = 0; m4 < 4; ++m4) {
+        const int m = 4 * wave + m4;  // 16 loads per tensor and tile, 4 per wavefront
+        int u = dma_row<kFwdKeys>(m, lane);
+        u = u < nrow ? u : nrow - 1;
+        const uint32_t off = (uint32_t)(u * (int)kv_row_stride + dma_col<kFwdKeys>(m, lane)) * 2u;
+        dma16_async(kb, off, kd + dma_dst_bytes<kFwdKeys>(m));
+        dma16_async(vb, off, vd + dma_dst_bytes<kFwdKeys>(m));
       }
     };
-    walk_kv_tiles(p, seq, tile.kvh, Pmax, wave, lane, kvbuf, [&](int j, int kv0, const bf16* ks, const bf16* vs) {
-      if (kv0 + kFwdKeys <= visible_keys(Pmin, j, p.C, seq.c)) compute(j, kv0, ks, vs, std::false_type{});
-      else compute(j, kv0, ks, vs, std::true_type{});
-    });
+
+    // ---- S^T of a tile: fragment f = 8 kb + c (keys 32 kb.., dims 16 c..)
+    // feeds both row blocks
+    auto s_frag = [&](const bf16* ks, int f) -> bf16x8 {
+      return ld16(&ks[tile_off<kFwdKeys>(32 * (f >> 3) + qi, 16 * (f & 7) + 8 * half)]);
+    };
+    auto s_mfma = [&](f32x16 (&S)[2][2], int f, int rb, const bf16x8& a) {
+      const int kb = f >> 3, c = f & 7;
+      if (c == 0) mfma32_v_first(S[rb][kb], a, qreg[rb][c]);
+      else mfma32_v(S[rb][kb], a, qreg[rb][c]);
+    };
+    // ---- O^T += V^T P^T: fragment g = 4 t4 + dt (keys 16 t4.., dims 32 dt..);
+    // a lane of half h holds keys 16 t4 + 4h + {0..3} and 16 t4 + 8 + 4h +
+    // {0..3} in its S^T registers and reads V^T from exactly those rows
+    auto v_frag = [&](const bf16* vs, int g) -> bf16x8 {
+      const int t4 = g >> 2, dt = g & 3;
+      return ld_tr8<kFwdKeys>(vs, 32 * dt, 16 * t4 + 4 * half, 16 * t4 + 8 + 4 * half, lane);
+    };
+
+    // row maximum of S^T (raw scores) over the 64 keys of a tile
+    auto tile_max = [&](const f32x16 (&S)[2][2], float (&mx)[2]) {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        float a = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) a = fmaxf(a, S[rb][kb][v]);
+        mx[rb] = fmaxf(a, xor32(a));
+      }
+    };
+
+    // ---- one pipelined iteration on tile t (scores Sc, V in buffer bc):
+    // S^T of tile t+1 (K in buffer bn) into Sn, softmax of tile t, then
+    // O^T += V^T P^T of tile t; the maximum of tile t+1 is taken at the end.
+    // MFMA j in slot j: j < 32 -> S^T fragment j/2, row block j%2;
+    // j >= 32 -> V^T fragment (j-32)/2, row block j%2.  Softmax element e
+    // (t4 = e/16, row block (e/8)%2, accumulator slot 8 (t4%2) + e%8 of key
+    // block t4/2) in slot 52e/64, ahead of the MFMAs of key block t4.
+    auto iterate = [&](f32x16 (&Sc)[2][2], f32x16 (&Sn)[2][2], const bf16* ks_n, const bf16* vs_c,
+                       const float (&m_eff)[2], float (&mx_n)[2]) {
+      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      bf16x8 fq[kFragAhead + 1];
+      bf16x2 pk[2][4][4];  // packed P^T: [row block][t4][pair]
+      float pv[2][4][8];
+      auto frag = [&](int f) -> bf16x8 { return f < 16 ? s_frag(ks_n, f) : v_frag(vs_c, f - 16); };
+      auto element = [&](int e) {
+        const int t4 = e >> 4, rb = (e >> 3) & 1, i = e & 7;
+        const float x = Sc[rb][t4 >> 1][8 * (t4 & 1) + i];
+        const float pr = fast_exp2(__builtin_fmaf(x, p.scale_log2, -m_eff[rb]));
+        pv[rb][t4][i] = pr;
+        lsum[rb] += pr;
+        if (i & 1) pk[rb][t4][i >> 1] = bf16x2{(bf16)pv[rb][t4][i - 1], (bf16)pr};
+      };
+      auto pa = [&](int rb, int t4) {
+        return bf16x8{pk[rb][t4][0][0], pk[rb][t4][0][1], pk[rb][t4][1][0], pk[rb][t4][1][1],
+                      pk[rb][t4][2][0], pk[rb][t4][2][1], pk[rb][t4][3][0], pk[rb][t4][3][1]};
+      };
+      static_for<kFragAhead>([&](auto fc) { fq[fc.value] = frag(fc.value); });
+      static_for<64>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        constexpr int f = j >> 1, rb = j & 1;
+        if constexpr (rb == 0 && f + kFragAhead < 32) fq[(f + kFragAhead) % (kFragAhead + 1)] = frag(f + kFragAhead);
+        static_for<64>([&](auto ec) {
+          constexpr int e = decltype(ec)::value;
+          if constexpr ((e * 52) / 64 == j) element(e);
+        });
+        if constexpr (j < 32) {
+          s_mfma(Sn, f, rb, fq[f % (kFragAhead + 1)]);
+        } else {
+          constexpr int g = f - 16, t4 = g >> 2, dt = g & 3;
+          mfma32_acc(o[rb][dt], fq[f % (kFragAhead + 1)], pa(rb, t4));
+        }
+        if constexpr (j == 63) tile_max(Sn, mx_n);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    };
+
+    // ---- apply the causal mask to the scores of a tile that needs it
+    auto mask_tile = [&](f32x16 (&S)[2][2], const KvCursor& c, float (&mx)[2]) {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        const int lim = valid[rb] ? visible_keys(tk[rb].P, c.j, p.C, seq.c) : 0;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int u = c.kv0 + 32 * kb + 8 * (v >> 2) + 4 * half + (v & 3);
+            if (u >= lim) S[rb][kb][v] = -INFINITY;
+          }
+      }
+      tile_max(S, mx);
+    };
+    // ---- new reference maxima; rescale O and the sums of rows whose
+    // maximum moved past the slack (rare after the first tiles)
+    auto update_max = [&](const float (&mx)[2], float (&m_eff)[2]) {
+      float m_new[2];
+      bool move[2];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        m_new[rb] = mx[rb] * p.scale_log2;  // the scale is positive
+        move[rb] = m_new[rb] > m_use[rb] + kRescaleSlack || (m_use[rb] == -INFINITY && m_new[rb] > -INFINITY);
+      }
+      if (__ballot(move[0] || move[1])) {
+        mfma_drain();  // pending O^T updates complete before the vector ALUs touch O
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+          const float alpha = move[rb] ? fast_exp2(m_use[rb] - m_new[rb]) : 1.f;  // m_use = -inf gives 0
+          if (move[rb]) m_use[rb] = m_new[rb];
+          lsum[rb] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt) acc_scale(o[rb][dt], alpha);
+        }
+        mfma_drain();
+      }
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) m_eff[rb] = m_use[rb] == -INFINITY ? 0.f : m_use[rb];
+    };
+
+    KvCursor cur = seek(p.step_first);
+    if (cur.i < step_end) {
+      KvCursor nxt = next(cur);
+      fetch(cur, 0);
+      if (nxt.i < step_end) fetch(nxt, 1);
+      __builtin_amdgcn_s_waitcnt(0);
+      lds_barrier();
+      f32x16 Sa[2][2], Sb[2][2];
+      float mx[2], m_eff[2];
+      // prologue: S^T of the first tile
+      static_for<32>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        s_mfma(Sa, j >> 1, j & 1, s_frag(&kvbuf[0][0][0], j >> 1));
+      });
+      mfma_drain();  // the scores are read by the vector ALUs next
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) vacc_settle(Sa[rb][kb]);
+      tile_max(Sa, mx);
+      int t = 0;
+      // tile t is in buffer t % 3; scores of tile t in Sa (t even) or Sb
+      auto step = [&](f32x16 (&Sc)[2][2], f32x16 (&Sn)[2][2]) {
+        const KvCursor n2 = next(nxt);
+        if (n2.i < step_end) fetch(n2, (t + 2) % kKvBufs);
+        if (cur.kv0 + kFwdKeys > visible_keys(Pmin, cur.j, p.C, seq.c)) mask_tile(Sc, cur, mx);
+        update_max(mx, m_eff);
+        // with no tile t+1 the S^T MFMAs read a stale buffer and are discarded
+        iterate(Sc, Sn, &kvbuf[(t + 1) % kKvBufs][0][0], &kvbuf[t % kKvBufs][1][0], m_eff, mx);
+        wait_vmcnt_lgkm0<0>();  // tile t+2 has landed for this wavefront
+        lds_barrier();
+        cur = nxt;
+        nxt = n2;
+        ++t;
+      };
+      while (true) {
+        step(Sa, Sb);
+        if (cur.i >= step_end) break;
+        step(Sb, Sa);
+        if (cur.i >= step_end) break;
+      }
+      mfma_drain();  // O^T complete before the epilogue reads it
+    }
   }
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) acc_settle(o[rb][dt]);
 
   // ------------------------------------------------------------ epilogues
-  const int64_t acc_row = (int64_t)(tile.tok_begin + tl) * p.hq + head;
+  // per row block; every lane runs both so cross-lane exchanges stay uniform
+  float l_tot[2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) l_tot[rb] = lsum[rb] + xor32(lsum[rb]);
 
-  if (MODE == kModeStep) {
-    const float l_tot = st.l + xor32(st.l);
-    if (!valid) return;
-    float* oacc = p.o_acc + acc_row * kHeadDim;
-    if (l_tot > 0.f) {
-      const float lse2 = st.m + __log2f(l_tot);
-      const float inv = 1.f / l_tot;
-      float wa = 0.f, wb = inv;
-      float lse_new = lse2;
-      if (!p.acc_first) {
-        const float la = p.lse_acc[acc_row];
-        const float hi = fmaxf(la, lse2);
-        const float ea = fast_exp2(la - hi);  // la = -inf gives 0
-        const float eb = fast_exp2(lse2 - hi);
-        const float tot = ea + eb;
-        lse_new = hi + __log2f(tot);
-        wa = ea / tot;
-        wb = eb / tot * inv;
+  auto finish = [&](int rb) {
+    const int64_t acc_row = (int64_t)(tile.tok_begin + (64 * wave + 32 * rb + qi) / p.G) * p.hq + head[rb];
+    f32x16 st_o[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) st_o[dt] = o[rb][dt];
+
+    if (MODE == kModeStep) {
+      if (!valid[rb]) return;
+      float* oacc = p.o_acc + acc_row * kHeadDim;
+      if (l_tot[rb] > 0.f) {
+        const float lse2 = m_use[rb] + __log2f(l_tot[rb]);
+        const float inv = 1.f / l_tot[rb];
+        float wa = 0.f, wb = inv;
+        float lse_new = lse2;
+        if (!p.acc_first) {
+          const float la = p.lse_acc[acc_row];
+          const float hi = fmaxf(la, lse2);
+          const float ea = fast_exp2(la - hi);  // la = -inf gives 0
+          const float eb = fast_exp2(lse2 - hi);
+          const float tot = ea + eb;
+          lse_new = hi + __log2f(tot);
+          wa = ea / tot;
+          wb = eb / tot * inv;
+        }
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+          for (int vq = 0; vq < 4; ++vq) {
+            float4* dst = reinterpret_cast<float4*>(oacc + 32 * dt + 8 * vq + 4 * half);
+            float4 prev = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (!p.acc_first) prev = *dst;
+            float4 r;
+            r.x = wa * prev.x + wb * st_o[dt][4 * vq + 0];
+            r.y = wa * prev.y + wb * st_o[dt][4 * vq + 1];
+            r.z = wa * prev.z + wb * st_o[dt][4 * vq + 2];
+            r.w = wa * prev.w + wb * st_o[dt][4 * vq + 3];
+            *dst = r;
+          }
+        }
+        if (half == 0) p.lse_acc[acc_row] = lse_new;
+      } else if (p.acc_first) {
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int vq = 0; vq < 4; ++vq)
+            *reinterpret_cast<float4*>(oacc + 32 * dt + 8 * vq + 4 * half) = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (half == 0) p.lse_acc[acc_row] = -INFINITY;
       }
+      return;
+    }
+
+    // main-sequence partial: normalised output in st_o, LSE (log2) in lse_m
+    float lse_m;
+    if (MODE == kModeFinal) {
+      if (valid[rb]) {
+        const float* oacc = p.o_acc + acc_row * kHeadDim;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int vq = 0; vq < 4; ++vq) {
+            const float4 a = *reinterpret_cast<const float4*>(oacc + 32 * dt + 8 * vq + 4 * half);
+            st_o[dt][4 * vq + 0] = a.x;
+            st_o[dt][4 * vq + 1] = a.y;
+            st_o[dt][4 * vq + 2] = a.z;
+            st_o[dt][4 * vq + 3] = a.w;
+          }
+        lse_m = p.lse_acc[acc_row];
+      } else {
+        lse_m = -INFINITY;
+      }
+    } else {
+      if (l_tot[rb] > 0.f) {
+        lse_m = m_use[rb] + __log2f(l_tot[rb]);
+        const float inv = 1.f / l_tot[rb];
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) st_o[dt] *= inv;
+      } else {
+        lse_m = -INFINITY;
+      }
+    }
+
+    // ---- branch-local partial (vector ALUs; at most 64 keys per row)
+    int nb = 0;
+    GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
+    if (valid[rb] && tk[rb].grp >= 0) {
+      gi = p.groups[tk[rb].grp];
+      nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk[rb].gidx + 1 : gi.len;
+    }
+    float mb = -INFINITY, lb = 0.f;
+    f32x16 ob[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) ob[dt] = f32x16{};
+    for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
+      const bool active = b < nb;
+      if (__ballot(active) == 0) break;
+      const int64_t krow = (int64_t)gi.row0 + (int64_t)b * gi.stride;
+      const bf16* kb = p.k_br + krow * kv_row_stride + tile.kvh * kHeadDim;
+      const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
+      float dot = 0.f;
+      if (active) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const bf16x8 kv = ld16(kb + 16 * c + 8 * half);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) dot += (float)qreg[rb][c][e] * (float)kv[e];
+        }
+      }
+      dot += xor32(dot);
+      if (!active) continue;
+      const float x = dot * p.scale_log2;
+      const float m_new = fmaxf(mb, x);
+      const float alpha = fast_exp2(mb - m_new);
+      const float e = fast_exp2(x - m_new);
+      lb = lb * alpha + e;
+      mb = m_new;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
         for (int vq = 0; vq < 4; ++vq) {
-          float4* dst = reinterpret_cast<float4*>(oacc + 32 * dt + 8 * vq + 4 * half);
-          float4 prev = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (!p.acc_first) prev = *dst;
-          float4 o;
-          o.x = wa * prev.x + wb * st.o[dt][4 * vq + 0];
-          o.y = wa * prev.y + wb * st.o[dt][4 * vq + 1];
-          o.z = wa * prev.z + wb * st.o[dt][4 * vq + 2];
-          o.w = wa * prev.w + wb * st.o[dt][4 * vq + 3];
-          *dst = o;
+          const bf16x4 vv = *reinterpret_cast<const bf16x4*>(vb + 32 * dt + 8 * vq + 4 * half);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) ob[dt][4 * vq + c] = ob[dt][4 * vq + c] * alpha + e * (float)vv[c];
         }
       }
-      if (half == 0) p.lse_acc[acc_row] = lse_new;
-    } else if (p.acc_first) {
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int vq = 0; vq < 4; ++vq)
-          *reinterpret_cast<float4*>(oacc + 32 * dt + 8 * vq + 4 * half) = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (half == 0) p.lse_acc[acc_row] = -INFINITY;
     }
-    return;
-  }
+    if (!valid[rb]) return;
 
-  // main-sequence partial: normalised output in st.o, LSE (log2) in lse_m
-  float lse_m;
-  if (MODE == kModeFinal) {
-    if (valid) {
-      const float* oacc = p.o_acc + acc_row * kHeadDim;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int vq = 0; vq < 4; ++vq) {
-          const float4 a = *reinterpret_cast<const float4*>(oacc + 32 * dt + 8 * vq + 4 * half);
-          st.o[dt][4 * vq + 0] = a.x;
-          st.o[dt][4 * vq + 1] = a.y;
-          st.o[dt][4 * vq + 2] = a.z;
-          st.o[dt][4 * vq + 3] = a.w;
-        }
-      lse_m = p.lse_acc[acc_row];
-    } else {
-      lse_m = -INFINITY;
-    }
-  } else {
-    const float l_tot = st.l + xor32(st.l);
-    if (l_tot > 0.f) {
-      lse_m = st.m + __log2f(l_tot);
-      const float inv = 1.f / l_tot;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) st.o[dt] *= inv;
-    } else {
-      lse_m = -INFINITY;
-    }
-  }
+    // ---- Eq. lse-merge of the main and branch partials, then write out
+    const float lse_b = lb > 0.f ? mb + __log2f(lb) : -INFINITY;
+    const float hi = fmaxf(lse_m, lse_b);
+    const float wm = lse_m == -INFINITY ? 0.f : fast_exp2(lse_m - hi);
+    const float wbr = lse_b == -INFINITY ? 0.f : fast_exp2(lse_b - hi);
+    const float tot = wm + wbr;
+    const float lse2 = hi + __log2f(tot);
+    const float cm = wm / tot;
+    const float cb = lb > 0.f ? wbr / (tot * lb) : 0.f;
 
-  // ---- branch-local partial (vector ALUs; at most 64 keys per row)
-  int nb = 0;
-  GroupInfo gi{0, 1, 0, 0};
-  if (valid && tk.grp >= 0) {
-    gi = p.groups[tk.grp];
-    nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk.gidx + 1 : gi.len;
-  }
-  float mb = -INFINITY, lb = 0.f;
-  f32x16 ob[4];
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt) ob[dt] = f32x16{};
-  for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
-    const bool active = b < nb;
-    if (__ballot(active) == 0) break;
-    const int64_t krow = (int64_t)gi.row0 + (int64_t)b * gi.stride;
-    const bf16* kb = p.k_br + krow * kv_row_stride + tile.kvh * kHeadDim;
-    const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
-    float dot = 0.f;
-    if (active) {
-#pragma unroll
-      for (int ks8 = 0; ks8 < 8; ++ks8) {
-        const bf16x8 kv = ld16(kb + 16 * ks8 + 8 * half);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) dot += (float)qreg[ks8][e] * (float)kv[e];
-      }
+    bf16* out;
+    float* lse_out;
+    if (tk[rb].qrow >= 0) {
+      out = p.o_main + ((int64_t)tk[rb].qrow * p.hq + head[rb]) * kHeadDim;
+      lse_out = p.lse_main + (int64_t)head[rb] * p.n_local + tk[rb].qrow;
+    } else {
+      const int64_t br = -tk[rb].qrow - 1;
+      out = p.o_br + (br * p.hq + head[rb]) * kHeadDim;
+      lse_out = p.lse_br + (int64_t)head[rb] * p.n_br + br;
     }
-    dot += xor32(dot);
-    if (!active) continue;
-    const float x = dot * p.scale_log2;
-    const float m_new = fmaxf(mb, x);
-    const float alpha = fast_exp2(mb - m_new);
-    const float e = fast_exp2(x - m_new);
-    lb = lb * alpha + e;
-    mb = m_new;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int vq = 0; vq < 4; ++vq) {
-        const bf16x4 vv = *reinterpret_cast<const bf16x4*>(vb + 32 * dt + 8 * vq + 4 * half);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) ob[dt][4 * vq + c] = ob[dt][4 * vq + c] * alpha + e * (float)vv[c];
+        const int v = 4 * vq;
+        *reinterpret_cast<bf16x4*>(out + 32 * dt + 8 * vq + 4 * half) =
+            pack4(cm * st_o[dt][v] + cb * ob[dt][v], cm * st_o[dt][v + 1] + cb * ob[dt][v + 1],
+                  cm * st_o[dt][v + 2] + cb * ob[dt][v + 2], cm * st_o[dt][v + 3] + cb * ob[dt][v + 3]);
       }
-    }
-  }
-  if (!valid) return;
-
-  // ---- Eq. lse-merge of the main and branch partials, then write out
-  const float lse_b = lb > 0.f ? mb + __log2f(lb) : -INFINITY;
-  const float hi = fmaxf(lse_m, lse_b);
-  const float wm = lse_m == -INFINITY ? 0.f : fast_exp2(lse_m - hi);
-  const float wbr = lse_b == -INFINITY ? 0.f : fast_exp2(lse_b - hi);
-  const float tot = wm + wbr;
-  const float lse2 = hi + __log2f(tot);
-  const float cm = wm / tot;
-  const float cb = lb > 0.f ? wbr / (tot * lb) : 0.f;
-
-  bf16* out;
-  float* lse_out;
-  if (tk.qrow >= 0) {
-    out = p.o_main + ((int64_t)tk.qrow * p.hq + head) * kHeadDim;
-    lse_out = p.lse_main + (int64_t)head * p.n_local + tk.qrow;
-  } else {
-    const int64_t br = -tk.qrow - 1;
-    out = p.o_br + (br * p.hq + head) * kHeadDim;
-    lse_out = p.lse_br + (int64_t)head * p.n_br + br;
-  }
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-    for (int vq = 0; vq < 4; ++vq) {
-      const int v = 4 * vq;
-      *reinterpret_cast<bf16x4*>(out + 32 * dt + 8 * vq + 4 * half) =
-          pack4(cm * st.o[dt][v] + cb * ob[dt][v], cm * st.o[dt][v + 1] + cb * ob[dt][v + 1],
-                cm * st.o[dt][v + 2] + cb * ob[dt][v + 2], cm * st.o[dt][v + 3] + cb * ob[dt][v + 3]);
-    }
-  if (half == 0) *lse_out = lse2 * kLn2;
+    if (half == 0) *lse_out = lse2 * kLn2;
+  };
+  finish(0);
+  finish(1);
 }
 
 hipError_t launch_fwd(const FwdParams& p, int mode, hipStream_t stream) {
