@@ -121,21 +121,23 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     };
     constexpr uint32_t kTileBytes = kFwdKeys * kHeadDim * sizeof(bf16);
     const uint32_t kv_lds = lds_addr(&kvbuf[0][0][0]);
-    auto fetch = [&](const KvCursor& c, int buf) {  // direct loads of tile c into buffer buf
+    // direct loads of tile c into buffer buf: 16 per tensor, 4 per
+    // wavefront; piece k = 2 m4 + tensor of this wavefront's eight
+    auto fetch_piece = [&](const KvCursor& c, int buf, int k) {
+      const int m4 = k >> 1, tensor = k & 1;
       const int64_t row0 = ((int64_t)seq.seg_off + c.kv0) * kv_row_stride + tile.kvh * kHeadDim;
-      const void* kb = uniform_ptr(p.k_step[c.j] + row0);
-      const void* vb = uniform_ptr(p.v_step[c.j] + row0);
-      const uint32_t kd = kv_lds + (uint32_t)(2 * buf) * kTileBytes, vd = kd + kTileBytes;
+      const void* base = uniform_ptr((tensor ? p.v_step[c.j] : p.k_step[c.j]) + row0);
+      const uint32_t dst = kv_lds + (uint32_t)(2 * buf + tensor) * kTileBytes;
       const int nrow = c.lim_hi - c.kv0;  // rows past the visible prefix repeat its last row
+      const int m = 4 * wave + m4;
+      int u = dma_row<kFwdKeys>(m, lane);
+      u = u < nrow ? u : nrow - 1;
+      const uint32_t off = (uint32_t)(u * (int)kv_row_stride + dma_col<kFwdKeys>(m, lane)) * 2u;
+      dma16_async(base, off, dst + dma_dst_bytes<kFwdKeys>(m));
+    };
+    auto fetch = [&](const KvCursor& c, int buf) {
 #pragma unroll
-      for (int m4 = 0; m4 < 4; ++m4) {
-        const int m = 4 * wave + m4;  // 16 loads per tensor and tile, 4 per wavefront
-        int u = dma_row<kFwdKeys>(m, lane);
-        u = u < nrow ? u : nrow - 1;
-        const uint32_t off = (uint32_t)(u * (int)kv_row_stride + dma_col<kFwdKeys>(m, lane)) * 2u;
-        dma16_async(kb, off, kd + dma_dst_bytes<kFwdKeys>(m));
-        dma16_async(vb, off, vd + dma_dst_bytes<kFwdKeys>(m));
-      }
+      for (int k = 0; k < 8; ++k) fetch_piece(c, buf, k);
     };
 
     // ---- S^T of a tile: fragment f = 8 kb + c (keys 32 kb.., dims 16 c..)
@@ -177,7 +179,7 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     // (t4 = e/16, row block (e/8)%2, accumulator slot 8 (t4%2) + e%8 of key
     // block t4/2) in slot 52e/64, ahead of the MFMAs of key block t4.
     auto iterate = [&](f32x16 (&Sc)[2][2], f32x16 (&Sn)[2][2], const bf16* ks_n, const bf16* vs_c,
-                       const float (&m_eff)[2], float (&mx_n)[2]) {
+                       const float (&m_eff)[2], float (&mx_n)[2], auto&& issue_piece) {
       typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
       bf16x8 fq[kFragAhead + 1];
       bf16x2 pk[2][4][4];  // packed P^T: [row block][t4][pair]
@@ -188,7 +190,7 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
         const float x = Sc[rb][t4 >> 1][8 * (t4 & 1) + i];
         const float pr = fast_exp2(__builtin_fmaf(x, p.scale_log2, -m_eff[rb]));
         pv[rb][t4][i] = pr;
-        lsum[rb] += pr;
+        lsum[rb] += pr;  // fp32 probabilities: the LSE bar is tighter than bf16 rounding
         if (i & 1) pk[rb][t4][i >> 1] = bf16x2{(bf16)pv[rb][t4][i - 1], (bf16)pr};
       };
       auto pa = [&](int rb, int t4) {
@@ -211,6 +213,7 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
           mfma32_acc(o[rb][dt], fq[f % (kFragAhead + 1)], pa(rb, t4));
         }
         if constexpr (j == 63) tile_max(Sn, mx_n);
+        if constexpr ((j & 7) == 4) issue_piece(j >> 3);  // direct loads of tile t+2, spread out
         __builtin_amdgcn_sched_barrier(0);
       });
     };
@@ -280,11 +283,14 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
       // tile t is in buffer t % 3; scores of tile t in Sa (t even) or Sb
       auto step = [&](f32x16 (&Sc)[2][2], f32x16 (&Sn)[2][2]) {
         const KvCursor n2 = next(nxt);
-        if (n2.i < step_end) fetch(n2, (t + 2) % kKvBufs);
+        // with no tile t+2 the loads repeat tile t into the idle buffer
+        const KvCursor ld = n2.i < step_end ? n2 : cur;
+        const int b2 = (t + 2) % kKvBufs;
         if (cur.kv0 + kFwdKeys > visible_keys(Pmin, cur.j, p.C, seq.c)) mask_tile(Sc, cur, mx);
         update_max(mx, m_eff);
         // with no tile t+1 the S^T MFMAs read a stale buffer and are discarded
-        iterate(Sc, Sn, &kvbuf[(t + 1) % kKvBufs][0][0], &kvbuf[t % kKvBufs][1][0], m_eff, mx);
+        iterate(Sc, Sn, &kvbuf[(t + 1) % kKvBufs][0][0], &kvbuf[t % kKvBufs][1][0], m_eff, mx,
+                [&](int k) { fetch_piece(ld, b2, k); });
         wait_vmcnt_lgkm0<0>();  // tile t+2 has landed for this wavefront
         lds_barrier();
         cur = nxt;

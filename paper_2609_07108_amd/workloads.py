@@ -146,9 +146,10 @@ def _groups_for(cu: np.ndarray, spec: Sequence[Tuple], rng: Optional[np.random.G
     """Lay out the branch groups of every sequence.
 
     ``spec[s]`` is ``None`` (no branches), ``("eagle", K)`` (one chain of K
-    tokens at every position) or ``("dflash", block, window)`` (one block of
-    ``block`` tokens per ``window`` positions, anchored at a uniform position
-    inside its window; anchors are drawn from ``rng`` in sequence order)."""
+    tokens at every position) or ``("dflash", block, window[, nblocks])``
+    (``nblocks``, default 1, blocks of ``block`` tokens per ``window``
+    positions, each anchored at a uniform position inside its window; anchors
+    are drawn from ``rng`` in sequence order, window by window)."""
     g_seq, g_anchor, g_kind, g_len = [], [], [], []
     for s, sp in enumerate(spec):
         L = int(cu[s + 1] - cu[s])
@@ -164,12 +165,13 @@ def _groups_for(cu: np.ndarray, spec: Sequence[Tuple], rng: Optional[np.random.G
             g_len.append(np.full(L, K))
         elif sp[0] == "dflash":
             block, window = int(sp[1]), int(sp[2])
+            nb = int(sp[3]) if len(sp) > 3 else 1
             nwin = L // window
-            offs = rng.integers(0, window, size=nwin)
-            g_seq.append(np.full(nwin, s))
-            g_anchor.append(np.arange(nwin) * window + offs)
-            g_kind.append(np.full(nwin, KIND_DFLASH))
-            g_len.append(np.full(nwin, block))
+            offs = rng.integers(0, window, size=nwin * nb) if nb > 1 else rng.integers(0, window, size=nwin)
+            g_seq.append(np.full(nwin * nb, s))
+            g_anchor.append(np.repeat(np.arange(nwin) * window, nb) + offs)
+            g_kind.append(np.full(nwin * nb, KIND_DFLASH))
+            g_len.append(np.full(nwin * nb, block))
         else:
             raise ValueError(sp)
     cat = lambda xs: (np.concatenate(xs).astype(np.int64) if xs else np.zeros(0, np.int64))

@@ -5,7 +5,10 @@ The cases span several query and key tiles with ragged tails, every GQA
 ratio the kernels tile differently (G = 1, 4, 8, 16), both branch kinds,
 both branch-array layouts, both ring schedules, context-parallel ranks at
 either end of the ring, an empty sequence, sequences without branches, fp32
-gradient output, and all-equal scores (Q = 0).
+gradient output, all-equal scores (Q = 0), and the mask variants of the
+draft families: DFlash/DSpark blocks of other sizes and several per window,
+DFlash with main queries, EAGLE depth per sequence up to the 64-member
+maximum.
 """
 
 import numpy as np
@@ -38,6 +41,14 @@ def case(name):
     if name == "edge_g1":
         return W.custom([0, 64, 8, 16], [None, ("eagle", 1), ("eagle", 2), None], hq=2, hkv=2,
                         cp_size=2, cp_rank=1, seed=205, name=name)
+    if name == "mask_variants":
+        # DFlash blocks of 8 (two per 32-position window) in a sequence that
+        # also has main queries, 32-token blocks in one that has none, and
+        # EAGLE chains of depth 1 and of the maximum 64 members
+        return W.custom([512, 384, 128, 64], [("dflash", 8, 32, 2), ("dflash", 32, 128), ("eagle", 1),
+                                              ("eagle", 64)],
+                        hq=16, hkv=4, cp_size=2, cp_rank=1, seed=207, has_main=[True, False, True, True],
+                        name=name)
     raise KeyError(name)
 
 
@@ -67,6 +78,7 @@ def test_config1_forward_every_rank(cuda, mode, r):
     ("dflash_g8", "group", torch.bfloat16),
     ("mixed_g16", "depth", torch.bfloat16),
     ("edge_g1", "group", torch.float32),
+    ("mask_variants", "depth", torch.bfloat16),
 ])
 def test_forward_backward_parity(cuda, mode, name, layout, grad_dtype):
     prob = case(name)
