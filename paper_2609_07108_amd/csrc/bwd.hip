@@ -343,9 +343,14 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
   // [buffer][K, V] plane tiles of 64 keys (see tile_off), double-buffered
   __shared__ __attribute__((aligned(16))) bf16 kvbuf[2][2][kFwdKeys * kHeadDim];
 
-  // two workgroups per query tile: rows [128 h, 128 h + 128) of it
-  const FwdTile tile = p.qtiles[blockIdx.x >> 1];
-  const int rbase = 128 * (blockIdx.x & 1);
+  // two workgroups per query tile, rows [128 h, 128 h + 128) of it.  Block
+  // 16 g + 8 h + x takes half h of tile 8 g + x: workgroups go to the 8 XCDs
+  // round-robin by index, so both halves of a tile run on one XCD and share
+  // its L2 for the K/V tiles they both stream
+  const int qt = 8 * (blockIdx.x >> 4) + (blockIdx.x & 7);
+  if (qt >= p.num_qtiles) return;
+  const FwdTile tile = p.qtiles[qt];
+  const int rbase = 128 * ((blockIdx.x >> 3) & 1);
   if (rbase / p.G >= tile.ntok) return;  // no token in this half
   const SeqInfo seq = p.seqs[tile.seq];
   const int tid = threadIdx.x;
@@ -608,7 +613,7 @@ hipError_t launch_bwd_kv(const BwdParams& p, hipStream_t stream) {
 
 hipError_t launch_bwd_dq(const BwdParams& p, int mode, hipStream_t stream) {
   if (p.num_qtiles == 0) return hipSuccess;
-  dim3 grid(2 * p.num_qtiles), block(256);
+  dim3 grid(16 * ((p.num_qtiles + 7) / 8)), block(256);  // see the block mapping in the kernel
   if (mode == kModeStep) hipLaunchKernelGGL(bwd_dq_kernel<kModeStep>, grid, block, 0, stream, p);
   else if (mode == kModeFinal) hipLaunchKernelGGL(bwd_dq_kernel<kModeFinal>, grid, block, 0, stream, p);
   else hipLaunchKernelGGL(bwd_dq_kernel<kModeFused>, grid, block, 0, stream, p);
