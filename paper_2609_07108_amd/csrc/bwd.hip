@@ -11,10 +11,12 @@
 // Kernels
 //   preprocess : Delta and LSE * log2(e) per (query token, head).
 //   kv         : dK and dV.  One workgroup per 128 keys of one ring-step
-//                block, sequence and KV head (dK/dV in registers); it walks
-//                the query tokens that reach those keys in 64-row tiles
-//                (tokens x the G heads of the KV head), double-buffered in
-//                LDS by direct global-to-LDS loads.  No atomics.
+//                block, sequence and KV head, as two wavefront pairs of 64
+//                keys (one wavefront of a pair computes P and dV, the other
+//                dS and dK, with P handed over in LDS); it walks the query
+//                tokens that reach those keys in 64-row tiles (tokens x the
+//                G heads of the KV head), prefetched into LDS by direct
+//                global-to-LDS loads.  No atomics.
 //   dq         : dQ, query-tile parallel like the forward: per key tile
 //                S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T, with the
 //                branch-local keys handled in the epilogue.  Splitting dQ off
@@ -46,8 +48,9 @@ __device__ __forceinline__ void store_grad(void* base, int64_t idx, float v, boo
 }  // namespace
 
 // ------------------------------------------------------------ preprocess
-// 32 lanes per (token, head): Delta = <dO, O> over 128 dims and the row's
-// LSE in log2 units; Q and dO rows are also copied into token order, so the
+// 32 lanes per (token, head): -Delta = -<dO, O> over 128 dims and the row's
+// LSE in log2 units (Delta is stored negated so the dK/dV kernel can start
+// its dP accumulation from it); Q and dO rows are also copied into token order, so the
 // dK/dV kernel addresses a query tile without indirection.
 __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
   const int64_t pair = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 5;
@@ -70,48 +73,80 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
   if (sub == 0) {
     const float lse = tk.qrow >= 0 ? p.lse_main[(int64_t)head * p.n_local + tk.qrow]
                                    : p.lse_br[(int64_t)head * p.n_br + (-tk.qrow - 1)];
-    p.rowstat[pair] = make_float2(lse * kLog2e, dlt);
+    p.rowstat[pair] = make_float2(lse * kLog2e, -dlt);
   }
 }
 
 // ------------------------------------------------------------ kv (ring)
 // Workgroup of 4 wavefronts (one per SIMD, up to 512 registers each) on 128
-// keys: wavefront w owns keys 32w..32w+31 against every 64-row query tile
-// (tokens x the G heads of the KV head).  K and V of its keys stay in
-// registers (B operands of S = Q K^T and dP = dO V^T), dK and dV accumulate
-// in registers.  No atomics.
+// keys, as two wavefront pairs of 64 keys: pair p owns keys 64p..64p+63.
+// Inside a pair the work of the four contractions is split by operand:
+//   score wavefront (w = p):     K of the pair's keys in registers;
+//                                S = Q K^T, P = exp2(S scale log2e - LSE
+//                                log2e) with the causal mask, P handed to
+//                                the partner through LDS, dV += P^T dO
+//   gradient wavefront (w = 2+p): V in registers; dP - Delta = dO V^T -
+//                                Delta (the accumulation starts from
+//                                -Delta), dS = P o (dP - Delta) with P read
+//                                back, dK += dS^T Q
+// Each wavefront runs 64 MFMAs per 64-row query tile and every Q or dO
+// operand fragment it reads from LDS feeds two of them (the pair's two
+// 32-key blocks), so the operand traffic per MFMA is half that of a
+// wavefront on 32 keys; the dK and dV accumulators of 64 keys (256
+// registers) sit in two register files.  No atomics.
 //
-// Query tiles (Q and dO plane tiles plus per-row LSE, Delta and causal
-// limit) rotate through three LDS buffers: while tile i is processed, tile
-// i+1 is resident and tile i+2 in flight.  Every global access of the loop
-// is such a direct load, at addresses computed from the token index alone
-// (token-ordered copies of Q and dO), so the loop has no compiler-visible
-// memory loads and the waits on the loads are explicit.
-//
-// Inside a stage the 64 MFMAs run in a fixed order -- S/dP of row block 0,
-// S/dP of row block 1, dV/dK over the four 16-row reduction blocks -- each
-// preceded by the LDS read of the operand kOpAhead MFMAs later and, from
-// the 17th on, by one softmax element, so that the exponentials overlap the
-// matrix work and no LDS latency is exposed.
+// Query tiles (tokens x the G heads of the KV head, ordered by causal limit)
+// are walked in order.  In stage i the score wavefronts compute P of tile
+// i+1 and dV of tile i (P of tile i kept in registers from stage i-1); the
+// gradient wavefronts compute dK of tile i with P of tile i written by their
+// partner in stage i-1.  One barrier per stage publishes P and the direct
+// loads.  Q of tile k (with per-row LSE and causal limit) is read in stages
+// k-1 and k and rotates through four LDS buffers; dO of tile k (with per-row
+// -Delta) is read in stage k and rotates through three; both are loaded two
+// stages before their first use by direct global-to-LDS loads, at addresses
+// computed from the token index alone (token-ordered copies of Q and dO), so
+// the loops have no compiler-visible memory loads and the waits on the loads
+// are explicit.  Inside a stage the MFMAs, their operand reads, the softmax
+// (or dS) elements and the P writes follow a fixed slot schedule.
 namespace {
 
 constexpr int kKvWaves = 4;
 constexpr int kKvThreads = 64 * kKvWaves;
-constexpr int kOpAhead = 4;
-constexpr int kDmaPerStage = 8;  // Q/dO direct loads of one wavefront per tile
+constexpr int kOpAhead = 2;  // operand fragments read ahead of their MFMAs (two MFMAs each)
+constexpr int kQBufs = 4;
+constexpr int kGBufs = 3;
 
-struct QTileLds {
+struct QSide {
   bf16 q[kBwdRows * kHeadDim];
-  bf16 g[kBwdRows * kHeadDim];
   float l2[kBwdRows];  // LSE * log2 e
-  float dl[kBwdRows];  // Delta
   int pl[kBwdRows];    // causal limit P (-1: no token)
 };
+struct GSide {
+  bf16 g[kBwdRows * kHeadDim];
+  float nd[kBwdRows];  // -Delta
+};
+struct KvLds {
+  QSide qs[kQBufs];
+  GSide gs[kGBufs];
+  // P of a tile as MFMA operand fragments: [tile parity][pair][4 rb + 2 kb
+  // + tt][lane] (rows 32 rb + 16 tt.., keys 32 kb.. of the pair)
+  bf16x8 x[2][2][8][64];
+};
+
+// slot of softmax element e (score wavefront) and of dS element e (gradient
+// wavefront) in a stage's 64-slot schedule
+// (score elements start 7 slots after the last S MFMA of row block 0: the
+// S MFMAs are inline assembly, so the compiler does not pad the 12 wait
+// states between them and a vector read of their result)
+constexpr int a_slot(int e) { return 22 + (e * 41) / 64; }
+constexpr int b_slot(int e) { return 17 + (e * 38) / 64; }
 
 }  // namespace
 
 __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
-  __shared__ __attribute__((aligned(16))) QTileLds qs[3];
+  __shared__ __attribute__((aligned(16))) KvLds sm;
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
   const BwdTile tile = p.tiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
@@ -120,6 +155,8 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform
   const int qi = lane & 31;
   const int half = lane >> 5;
+  const bool scorer = wave < 2;
+  const int pair = wave & 1;
   const int G = p.G;
   const int tpt = kBwdRows / G;  // tokens per query tile
   const int ntiles = (tile.q_end - tile.q_begin + tpt - 1) / tpt;  // >= 1 (planner)
@@ -127,211 +164,395 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   const int64_t key0 = (int64_t)seq.seg_off + tile.u0;  // first key row in the block
   const int head0 = tile.kvh * G;
 
-  // ---- this lane's key: its position decides visibility (visible to a row
-  // iff position <= the row's causal limit; local index < c lies in chunk
-  // `step`, the rest in chunk 2C-1-step)
-  const int my_key = 32 * wave + qi;
-  const int kload = my_key < tile.nk ? my_key : tile.nk - 1;
-  int kpos;
-  {
+  // ---- the lane's keys 64 pair + 32 kb + qi: the position decides
+  // visibility (visible to a row iff position <= the row's causal limit;
+  // local index < c lies in chunk `step`, the rest in chunk 2C-1-step)
+  int kpos[2], kload[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int my_key = 64 * pair + 32 * kb + qi;
+    kload[kb] = my_key < tile.nk ? my_key : tile.nk - 1;
     const int u = tile.u0 + my_key;
-    kpos = u < seq.c ? tile.step * seq.c + u : (2 * p.C - 1 - tile.step) * seq.c + (u - seq.c);
-    if (my_key >= tile.nk) kpos = 0x7fffffff;
+    kpos[kb] = u < seq.c ? tile.step * seq.c + u : (2 * p.C - 1 - tile.step) * seq.c + (u - seq.c);
+    if (my_key >= tile.nk) kpos[kb] = 0x7fffffff;
   }
 
-  // ---- direct-load rows: lane carries tile rows 32*(w%2) + 16j + lane/4
-  // (j = 0, 1) of Q (wavefronts 0-1) or dO (2-3); wavefronts 0-2 also load
-  // one statistic of row `lane`.  Rows without a token read the tile's first
-  // row (finite data) and the sentinel token's limit -1.
-  const bf16* src = wave >= 2 ? p.gtok : p.qtok;
+  // ---- direct loads: the score wavefronts load Q rows 32 w + 16 j + lane/4
+  // (j = 0, 1), the gradient wavefronts the same rows of dO; wavefront 0
+  // also loads the tile's LSE, 1 its causal limits, 2 its -Delta.  Rows
+  // without a token read the tile's first row (finite data) and the
+  // sentinel token's limit -1.
   int dtl[2], dhg[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    const int row = 32 * (wave & 1) + 16 * j + (lane >> 2);
+    const int row = 32 * pair + 16 * j + (lane >> 2);
     dtl[j] = row / G;
     dhg[j] = row - dtl[j] * G;
   }
   const int stl = lane / G, shg = lane - stl * G;
-  const uint32_t qs_lds = lds_addr(&qs[0]);
-  auto issue = [&](int t) {
-    const uint32_t b = qs_lds + (uint32_t)(t % 3) * (uint32_t)sizeof(QTileLds);
-    // past the end: the last tile again, into the idle buffer
-    const int qt0 = tile.q_begin + (t < ntiles ? t : ntiles - 1) * tpt;
-    const int nt = tile.q_end - qt0;  // tokens left from qt0
-    if (wave < 3) {
-      const bool ok = stl < tpt && stl < nt;
-      if (wave == 2) {
-        const void* base = uniform_ptr(p.toks + qt0);
-        const uint32_t off = (uint32_t)((ok ? stl : p.num_tokens - qt0) * (int)sizeof(TokInfo) +
+  const uint32_t q_lds = lds_addr(&sm.qs[0]);
+  const uint32_t g_lds = lds_addr(&sm.gs[0]);
+  // Q of tile kq (score wavefronts) or dO of tile kg (gradient wavefronts);
+  // past the last tile the last one again, into the tile's own (idle)
+  // buffer.  A stage's loads go out in 9 pieces spread over its schedule:
+  // pieces 0-7 are the row loads (rows 32 pair + 16 (piece/4) + lane/4,
+  // plane piece%4), piece 8 the statistic.
+  const bf16* rows_src = scorer ? p.qtok : p.gtok;
+  asm volatile("" : "+s"(rows_src));  // kept in registers, not re-read per stage
+  struct DmaStage {
+    int qt0, nt;
+    uint32_t b;
+  };
+  auto dma_begin = [&](int kq, int kg) __attribute__((always_inline)) {
+    const int k = scorer ? kq : kg;
+    DmaStage d;
+    d.qt0 = tile.q_begin + (k < ntiles ? k : ntiles - 1) * tpt;
+    d.nt = tile.q_end - d.qt0;  // tokens left from qt0
+    d.b = scorer ? q_lds + (uint32_t)(k % kQBufs) * (uint32_t)sizeof(QSide)
+                 : g_lds + (uint32_t)(k % kGBufs) * (uint32_t)sizeof(GSide);
+    return d;
+  };
+  auto dma_piece = [&](const DmaStage& d, int piece) __attribute__((always_inline)) {
+    if (piece == 8) {
+      const bool ok = stl < tpt && stl < d.nt;
+      if (wave == 1) {
+        const void* base = uniform_ptr(p.toks + d.qt0);
+        const uint32_t off = (uint32_t)((ok ? stl : p.num_tokens - d.qt0) * (int)sizeof(TokInfo) +
                                         (int)offsetof(TokInfo, P));
-        dma4_async(base, off, b + (uint32_t)offsetof(QTileLds, pl));
-      } else {
-        const void* base = uniform_ptr(p.rowstat + (int64_t)qt0 * p.hq + head0);
-        const uint32_t off = (uint32_t)((ok ? stl * p.hq + shg : 0) * (int)sizeof(float2) + 4 * wave);
-        dma4_async(base, off, b + (uint32_t)(wave == 0 ? offsetof(QTileLds, l2) : offsetof(QTileLds, dl)));
+        dma4_async(base, off, d.b + (uint32_t)offsetof(QSide, pl));
+      } else if (wave != 3) {
+        const void* base = uniform_ptr(p.rowstat + (int64_t)d.qt0 * p.hq + head0);
+        const uint32_t off = (uint32_t)((ok ? stl * p.hq + shg : 0) * (int)sizeof(float2) + (wave == 0 ? 0 : 4));
+        dma4_async(base, off, d.b + (uint32_t)(wave == 0 ? offsetof(QSide, l2) : offsetof(GSide, nd)));
       }
+      return;
     }
-    const uint32_t dst = b + (uint32_t)(wave >= 2 ? offsetof(QTileLds, g) : offsetof(QTileLds, q));
-    const void* base = uniform_ptr(src + ((int64_t)qt0 * p.hq + head0) * kHeadDim);
+    const int j = piece >> 2, pl = piece & 3;
+    const void* base = uniform_ptr(rows_src + ((int64_t)d.qt0 * p.hq + head0) * kHeadDim);
+    const bool okr = dtl[j] < tpt && dtl[j] < d.nt;
+    const int r = okr ? dtl[j] * p.hq + dhg[j] : 0;  // row relative to (qt0, head0)
+    const int m = 8 * pair + 4 * j + pl;
+    const uint32_t off = (uint32_t)(r * kHeadDim + dma_col<kBwdRows>(m, lane)) * (uint32_t)sizeof(bf16);
+    dma16_async(base, off, d.b + dma_dst_bytes<kBwdRows>(m));  // q and g open both sides
+  };
+  auto issue_all = [&](int kq, int kg) __attribute__((always_inline)) {
+    const DmaStage d = dma_begin(kq, kg);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const bool ok = dtl[j] < tpt && dtl[j] < nt;
-      const int r = ok ? dtl[j] * p.hq + dhg[j] : 0;  // row relative to (qt0, head0)
-#pragma unroll
-      for (int pl = 0; pl < 4; ++pl) {
-        const int m = 8 * (wave & 1) + 4 * j + pl;
-        const uint32_t off = (uint32_t)(r * kHeadDim + dma_col<kBwdRows>(m, lane)) * (uint32_t)sizeof(bf16);
-        dma16_async(base, off, dst + dma_dst_bytes<kBwdRows>(m));
-      }
-    }
+    for (int piece = 0; piece < 9; ++piece) dma_piece(d, piece);
+  };
+  // End of a stage: this wavefront's loads issued before the stage (the
+  // tiles the next stage reads) have landed and its P writes are done; the
+  // loads of this stage (9 for wavefronts 0-2, 8 for wavefront 3) stay in
+  // flight.  The barrier publishes everything to the workgroup.
+  auto stage_end = [&]() __attribute__((always_inline)) {
+    if (wave == 3) wait_vmcnt_lgkm0<8>();
+    else wait_vmcnt_lgkm0<9>();
+    lds_barrier();
   };
 
-  bf16x8 kreg[8], vreg[8];
-  {
-    const bf16* kp = p.k_step[tile.step] + (key0 + kload) * kv_row_stride + tile.kvh * kHeadDim;
-    const bf16* vp = p.v_step[tile.step] + (key0 + kload) * kv_row_stride + tile.kvh * kHeadDim;
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      kreg[c] = ld16(kp + 16 * c + 8 * half);
-      vreg[c] = ld16(vp + 16 * c + 8 * half);
-    }
-  }
-  f32x16 dk[4], dv[4];
-#pragma unroll
-  for (int nt = 0; nt < 4; ++nt) {
-    mfma32_acc_zero(dk[nt]);
-    mfma32_acc_zero(dv[nt]);
-  }
-  issue(0);
-  issue(1);
-  __builtin_amdgcn_s_waitcnt(0);
-  lds_barrier();
-
-  // ---- the stage.  MFMA j: j < 32 -> S (even j) / dP (odd j) of row block
-  // j/16, reduction chunk (j/2)%8; j >= 32 -> dV (even) / dK (odd), column
-  // block ((j-32)/2)%4, reduction block t = (j-32)/8 (query rows 16t..16t+15;
-  // a lane of half h holds rows 16t+4h+{0..3} and 16t+8+4h+{0..3}, so the
-  // dO / Q operand is read column-wise from the same rows).
-  // Softmax element e (slot 16+e): accumulator slot e%16 of row block e/16,
-  // query row 32(e/16) + 8((e%16)/4) + 4h + e%4.
-  auto stage = [&](const QTileLds& cur, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    f32x16 s[2], dp[2];
-    bf16x8 opq[kOpAhead + 1];
-    float4 sl[8], sd[8];
-    int4 sp[8];
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    bf16x2 pp[16], pd[16];
-    float prv = 0.f, dsv = 0.f;
-
-    auto load_op = [&](int j) -> bf16x8 {
-      if (j < 32) {
-        const int off = tile_off<kBwdRows>(32 * (j >> 4) + qi, 16 * ((j >> 1) & 7) + 8 * half);
-        return ld16((j & 1) ? &cur.g[off] : &cur.q[off]);
-      }
-      const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3;
-      return ld_tr8<kBwdRows>((jj & 1) ? cur.q : cur.g, 32 * nt, 16 * t + 4 * half, 16 * t + 8 + 4 * half,
-                              lane);
-    };
-    auto load_stats = [&](int q) {
-      const int r0 = 32 * (q >> 2) + 8 * (q & 3) + 4 * half;
-      sl[q] = *reinterpret_cast<const float4*>(&cur.l2[r0]);
-      sd[q] = *reinterpret_cast<const float4*>(&cur.dl[r0]);
-      if (MASK) sp[q] = *reinterpret_cast<const int4*>(&cur.pl[r0]);
-    };
-    auto softmax = [&](int e) {
-      const int mt = e >> 4, v = e & 15, q = e >> 2, c = e & 3;
-      const float l = c == 0 ? sl[q].x : c == 1 ? sl[q].y : c == 2 ? sl[q].z : sl[q].w;
-      const float d = c == 0 ? sd[q].x : c == 1 ? sd[q].y : c == 2 ? sd[q].z : sd[q].w;
-      float pr = fast_exp2(__builtin_fmaf(s[mt][v], p.scale_log2, -l));
-      if (MASK) {
-        const int lim = c == 0 ? sp[q].x : c == 1 ? sp[q].y : c == 2 ? sp[q].z : sp[q].w;
-        pr = kpos <= lim ? pr : 0.f;
-      }
-      const float ds = pr * (dp[mt][v] - d);
-      if (e & 1) {
-        pp[e >> 1] = bf16x2{(bf16)prv, (bf16)pr};
-        pd[e >> 1] = bf16x2{(bf16)dsv, (bf16)ds};
-      } else {
-        prv = pr;
-        dsv = ds;
-      }
-    };
-    auto pa = [&](int t) {
-      return bf16x8{pp[4 * t][0], pp[4 * t][1], pp[4 * t + 1][0], pp[4 * t + 1][1],
-                    pp[4 * t + 2][0], pp[4 * t + 2][1], pp[4 * t + 3][0], pp[4 * t + 3][1]};
-    };
-    auto dsa = [&](int t) {
-      return bf16x8{pd[4 * t][0], pd[4 * t][1], pd[4 * t + 1][0], pd[4 * t + 1][1],
-                    pd[4 * t + 2][0], pd[4 * t + 2][1], pd[4 * t + 3][0], pd[4 * t + 3][1]};
-    };
-    auto mfma = [&](int j, const bf16x8& a) {
-      if (j < 32) {
-        const int mt = j >> 4, c = (j >> 1) & 7;
-        if (j & 1) dp[mt] = mfma32(a, vreg[c], c ? dp[mt] : f32x16{});
-        else s[mt] = mfma32(a, kreg[c], c ? s[mt] : f32x16{});
-      } else {
-        const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3;
-        if (jj & 1) mfma32_acc(dk[nt], dsa(t), a);
-        else mfma32_acc(dv[nt], pa(t), a);
-      }
-    };
-
-    static_for<kOpAhead>([&](auto jc) { opq[jc.value] = load_op(jc.value); });
-    static_for<64>([&](auto jc) {
-      constexpr int j = decltype(jc)::value;
-      if constexpr (j + kOpAhead < 64) opq[(j + kOpAhead) % (kOpAhead + 1)] = load_op(j + kOpAhead);
-      if constexpr (j >= 12 && j < 44 && (j & 3) == 0) load_stats((j - 12) >> 2);
-      if constexpr (j >= 16 && j < 48) softmax(j - 16);
-      mfma(j, opq[j % (kOpAhead + 1)]);
-      __builtin_amdgcn_sched_barrier(0);
-    });
+  // Operand fragments of a 64-row plane tile sit at compile-time offsets
+  // from four per-lane bases: row fragments (rows 32 rb + qi, columns
+  // 16 c + 8h; the chunk permutation depends on c only through its parity)
+  // from row_even / row_odd, transposed fragments (rows 16 t + 4h + {0..3}
+  // and 16 t + 8 + 4h + {0..3}, columns 32 nt + ..) from tr_lo / tr_hi.
+  const int row_even = tile_off<kBwdRows>(qi, 8 * half);
+  const int row_odd = tile_off<kBwdRows>(qi, 16 + 8 * half);
+  const int trc = (lane & 16) + 4 * (lane & 3);
+  const int tr_lo = tile_off<kBwdRows>(4 * half + ((lane & 15) >> 2), trc);
+  const int tr_hi = tile_off<kBwdRows>(8 + 4 * half + ((lane & 15) >> 2), trc);
+  // A stage's four bases (LDS byte addresses) are opaque to the compiler, so
+  // it cannot re-associate the constant offsets into per-fragment registers.
+  struct OpBases {
+    uint32_t re, ro, tl, th;
+  };
+  auto op_bases = [&](const bf16* rowT, const bf16* trT) __attribute__((always_inline)) {
+    OpBases o{lds_lane_addr(rowT + row_even), lds_lane_addr(rowT + row_odd), lds_lane_addr(trT + tr_lo),
+              lds_lane_addr(trT + tr_hi)};
+    asm volatile("" : "+v"(o.re), "+v"(o.ro), "+v"(o.tl), "+v"(o.th));
+    return o;
+  };
+  auto row_frag = [&](const OpBases& o, int rb, int c) __attribute__((always_inline)) {
+    return lds_ld16(((c & 1) ? o.ro : o.re) + (uint32_t)(((c >> 1) * kBwdRows + 32 * rb) * 64));
+  };
+  auto tr_frag = [&](const OpBases& o, int t, int nt) __attribute__((always_inline)) {
+    const uint32_t off = (uint32_t)((nt * kBwdRows + 16 * t) * 64);
+    const bf16x4 lo = lds_ld_tr4(o.tl + off), hi = lds_ld_tr4(o.th + off);
+    return bf16x8(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
 
   // Tiles [t_lo, t_hi) need no mask: every row has a token and sees all
-  // keys of the block (tokens from q_full on do).  The three ranges run as
-  // separate loops so each has one stage variant and the accumulators stay
-  // in place across iterations.
+  // keys of the block (tokens from q_full on do).
   int t_lo = ntiles, t_hi = ntiles;
   if (tile.nk == kBwdKeys && tpt * G == kBwdRows) {
     t_lo = min(ntiles, max(0, (tile.q_full - tile.q_begin + tpt - 1) / tpt));
     t_hi = max(t_lo, (tile.q_end - tile.q_begin) / tpt);
   }
-  auto run = [&](int t0, int t1, auto mask_tag) {
-    for (int it = t0; it < t1; ++it) {
-      issue(it + 2);
-      stage(qs[it % 3], mask_tag);
-      // tile it+1 (issued one stage ago) has landed for this wavefront; the
-      // loads of tile it+2 stay in flight
-      wait_vmcnt_lgkm0<kDmaPerStage>();
-      lds_barrier();
-    }
-    mfma_drain();  // accumulators settled before the compiler may move them
+
+  // Q of tiles 0 and 1, dO of tile 0
+  issue_all(0, 0);
+  if (scorer) issue_all(1, 0);
+  f32x16 acc[2][4];  // dV (score) or dK (gradient): [kb][d block], rows = keys, lane = dim
+  auto zero_acc = [&]() {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) mfma32_acc_zero(acc[kb][nt]);
   };
-  run(0, t_lo, std::true_type{});
-  run(t_lo, t_hi, std::false_type{});
-  run(t_hi, ntiles, std::true_type{});
+  const bf16* kvsrc = (scorer ? p.k_step[tile.step] : p.v_step[tile.step]) + tile.kvh * kHeadDim;
+
+  if (scorer) {
+    // K of the lane's keys (B operands of S = Q K^T), resident in the
+    // accumulation registers
+    bf16x8 kreg[2][8];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) load16_agpr(kreg[kb][c], kvsrc + (key0 + kload[kb]) * kv_row_stride + 16 * c + 8 * half);
+    zero_acc();
+    __builtin_amdgcn_s_waitcnt(0);
+    lds_barrier();
+    // ---------------------------------------------------------- score side
+    // stage: S and P of the next tile (Q, LSE, limits in qn; P fragments
+    // out to pn and to the exchange slot xw), dV of the current tile (dO in
+    // gc, its P in pc).  MFMA j: j < 32 -> S[rb][kb] chunk c (rb = j/16,
+    // c = (j/2)%8, kb = j%2); j >= 32 -> dV[kb][nt] with rows 16t.. (t =
+    // (j-32)/8, nt = ((j-32)/2)%4, kb = j%2).  Operand fragment j/2 feeds
+    // MFMAs j and j+1.
+    typedef u32x4 PFrags[2][2][2];  // P as bf16 pairs: [rb][kb][tt]
+    auto stage = [&](const QSide& qn, const GSide& gc, const PFrags& pc, PFrags& pn, bf16x8* xw, const DmaStage& dm,
+                     auto mask_tag, auto next_tag, auto cur_tag) __attribute__((always_inline)) {
+      constexpr bool MASK = decltype(mask_tag)::value;
+      constexpr bool NEXT = decltype(next_tag)::value;
+      constexpr bool CUR = decltype(cur_tag)::value;
+      constexpr int f_lo = NEXT ? 0 : 16, f_hi = CUR ? 32 : 16;
+      f32x16 s[2][2];
+      bf16x8 opq[kOpAhead + 1];
+      float4 sl[2][4];
+      int4 sp[2][4];
+      float prv = 0.f;
+
+      const OpBases ob = op_bases(qn.q, gc.g);
+      auto load_op = [&](int f) -> bf16x8 {
+        if (f < 16) return row_frag(ob, f >> 3, f & 7);
+        // rows 16t+4h+{0..3}, 16t+8+4h+{0..3}: the rows of the lane's P values
+        return tr_frag(ob, (f - 16) >> 2, (f - 16) & 3);
+      };
+      auto load_stats = [&](int rb, int q) {
+        const int r0 = 32 * rb + 8 * q + 4 * half;
+        sl[rb][q] = *reinterpret_cast<const float4*>(&qn.l2[r0]);
+        if (MASK) sp[rb][q] = *reinterpret_cast<const int4*>(&qn.pl[r0]);
+      };
+      // element e: rb = e/32, q = (e/8)%4, kb = (e/4)%2, accumulator slot
+      // v = 4q + e%4 (row 32 rb + 8q + 4h + e%4)
+      auto element = [&](int e) {
+        const int rb = e >> 5, q = (e >> 3) & 3, kb = (e >> 2) & 1, c = e & 3, v = 4 * q + c;
+        const float l = c == 0 ? sl[rb][q].x : c == 1 ? sl[rb][q].y : c == 2 ? sl[rb][q].z : sl[rb][q].w;
+        float pr = fast_exp2(__builtin_fmaf(s[rb][kb][v], p.scale_log2, -l));
+        if (MASK) {
+          const int lim = c == 0 ? sp[rb][q].x : c == 1 ? sp[rb][q].y : c == 2 ? sp[rb][q].z : sp[rb][q].w;
+          pr = kpos[kb] <= lim ? pr : 0.f;
+        }
+        if (v & 1) pn[rb][kb][v >> 3][(v & 7) >> 1] = __builtin_bit_cast(uint32_t, bf16x2{(bf16)prv, (bf16)pr});
+        else prv = pr;
+      };
+      auto mfma = [&](int j, const bf16x8& a) {
+        if (j < 32) {
+          const int rb = j >> 4, c = (j >> 1) & 7, kb = j & 1;
+          if (c == 0) mfma32_v_first(s[rb][kb], a, kreg[kb][c]);
+          else mfma32_v(s[rb][kb], a, kreg[kb][c]);
+        } else {
+          const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3, kb = jj & 1;
+          mfma32_acc(acc[kb][nt], __builtin_bit_cast(bf16x8, pc[t >> 1][kb][t & 1]), a);
+        }
+      };
+
+      static_for<kOpAhead>([&](auto ic) {
+        constexpr int f = f_lo + decltype(ic)::value;
+        if constexpr (f < f_hi) opq[f % (kOpAhead + 1)] = load_op(f);
+      });
+      static_for<64>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        constexpr int f = j >> 1;
+        constexpr bool active = f >= f_lo && f < f_hi;
+        if constexpr (active && (j & 1) == 0 && f + kOpAhead < f_hi)
+          opq[(f + kOpAhead) % (kOpAhead + 1)] = load_op(f + kOpAhead);
+        if constexpr (NEXT) {
+          // statistics of rows 32 rb + 8 q + 4h.. three slots before their elements
+          static_for<8>([&](auto gc_) {
+            constexpr int g = decltype(gc_)::value;
+            if constexpr (a_slot(8 * g) - 3 == j) load_stats(g >> 2, g & 3);
+          });
+          static_for<64>([&](auto ec) {
+            constexpr int e = decltype(ec)::value;
+            if constexpr (a_slot(e) == j) element(e);
+          });
+          // a fragment (rows 32 rb + 16 tt.., keys 32 kb..) is complete with
+          // its element of q = 2 tt + 1, c = 3
+          static_for<8>([&](auto fc) {
+            constexpr int fr = decltype(fc)::value;
+            constexpr int rb = fr >> 2, kb = (fr >> 1) & 1, tt = fr & 1;
+            if constexpr (a_slot(32 * rb + 8 * (2 * tt + 1) + 4 * kb + 3) + 1 == j)
+              xw[fr * 64 + lane] = __builtin_bit_cast(bf16x8, pn[rb][kb][tt]);
+          });
+        }
+        if constexpr (active) mfma(j, opq[f % (kOpAhead + 1)]);
+        if constexpr (j == 2) dma_piece(dm, 8);
+        if constexpr ((j & 7) == 4) dma_piece(dm, j >> 3);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    };
+
+    PFrags pa, pb;  // P of the current tile in pa between stages
+    int s = 0;
+    // one stage s: P of tile s+1 (mask class given), dV of tile s
+    auto one = [&](const PFrags& pc, PFrags& pn, auto mask_tag) __attribute__((always_inline)) {
+      stage(sm.qs[(s + 1) % kQBufs], sm.gs[s % kGBufs], pc, pn, &sm.x[(s + 1) & 1][pair][0][0], dma_begin(s + 3, s + 2),
+            mask_tag, std::true_type{}, std::true_type{});
+      stage_end();
+      ++s;
+    };
+    // stages [s, s_end), all of one mask class
+    auto run = [&](int s_end, auto mask_tag) __attribute__((always_inline)) {
+      while (s + 1 < s_end) {
+        one(pa, pb, mask_tag);
+        one(pb, pa, mask_tag);
+      }
+      if (s < s_end) {
+        one(pa, pb, mask_tag);
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) pa[rb][kb][tt] = pb[rb][kb][tt];
+      }
+      mfma_drain();  // accumulators settled before the compiler may move them
+    };
+
+    // stage -1: P of tile 0 only
+    if (t_lo == 0 && t_hi > 0)
+      stage(sm.qs[0], sm.gs[0], pb, pa, &sm.x[0][pair][0][0], dma_begin(2, 1), std::false_type{}, std::true_type{},
+            std::false_type{});
+    else
+      stage(sm.qs[0], sm.gs[0], pb, pa, &sm.x[0][pair][0][0], dma_begin(2, 1), std::true_type{}, std::true_type{},
+            std::false_type{});
+    stage_end();
+    // stages 0 .. ntiles-2 by the mask class of their next tile, then the last
+    run(min(ntiles - 1, max(0, t_lo - 1)), std::true_type{});
+    run(min(ntiles - 1, max(0, t_hi - 1)), std::false_type{});
+    run(ntiles - 1, std::true_type{});
+    stage(sm.qs[0], sm.gs[s % kGBufs], pa, pb, &sm.x[0][pair][0][0], dma_begin(s + 3, s + 2), std::true_type{},
+          std::false_type{}, std::true_type{});
+    stage_end();
+    mfma_drain();
+  } else {
+    // ------------------------------------------------------- gradient side
+    bf16x8 vreg[2][8];  // V of the lane's keys: B operands of dP = dO V^T
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) vreg[kb][c] = ld16(kvsrc + (key0 + kload[kb]) * kv_row_stride + 16 * c + 8 * half);
+    zero_acc();
+    __builtin_amdgcn_s_waitcnt(0);
+    lds_barrier();
+
+    // stage: dP - Delta and dS of the current tile (dO and -Delta in gc, P
+    // from the exchange slot xr), dK with Q in qc.  MFMA j: j < 32 ->
+    // dP[rb][kb] chunk c (as S on the score side); j >= 32 -> dK[kb][nt]
+    // with rows 16t.. .  dS element e runs chunk-major: t = e/16 (rows
+    // 16t.., accumulator slots 8 (t%2)..), kb = (e/8)%2, slot 8 (t%2) + e%8.
+    auto stage = [&](const QSide& qc, const GSide& gc, const bf16x8* xr, const DmaStage& dm) __attribute__((always_inline)) {
+      f32x16 dp[2][2], nd[2];
+      bf16x8 opq[kOpAhead + 1];
+      bf16x8 pf[2][2][2];  // P fragments [rb][kb][tt]
+      u32x4 dsf[2][2][2];  // dS as bf16 pairs, the A operands of dK: [rb][kb][tt]
+      float dsv = 0.f;
+
+      const OpBases ob = op_bases(gc.g, qc.q);
+      auto load_op = [&](int f) -> bf16x8 {
+        if (f < 16) return row_frag(ob, f >> 3, f & 7);
+        return tr_frag(ob, (f - 16) >> 2, (f - 16) & 3);
+      };
+      auto load_nd = [&](int rb) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 d4 = *reinterpret_cast<const float4*>(&gc.nd[32 * rb + 8 * q + 4 * half]);
+          nd[rb][4 * q] = d4.x;
+          nd[rb][4 * q + 1] = d4.y;
+          nd[rb][4 * q + 2] = d4.z;
+          nd[rb][4 * q + 3] = d4.w;
+        }
+      };
+      auto element = [&](int e) {
+        const int t = e >> 4, rb = t >> 1, tt = t & 1, kb = (e >> 3) & 1, i = e & 7, v = 8 * tt + i;
+        const float ds = (float)pf[rb][kb][tt][i] * dp[rb][kb][v];
+        if (i & 1) dsf[rb][kb][tt][i >> 1] = __builtin_bit_cast(uint32_t, bf16x2{(bf16)dsv, (bf16)ds});
+        else dsv = ds;
+      };
+      auto mfma = [&](int j, const bf16x8& a) {
+        if (j < 32) {
+          const int rb = j >> 4, c = (j >> 1) & 7, kb = j & 1;
+          dp[rb][kb] = mfma32(a, vreg[kb][c], c ? dp[rb][kb] : nd[rb]);
+        } else {
+          const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3, kb = jj & 1;
+          mfma32_acc(acc[kb][nt], __builtin_bit_cast(bf16x8, dsf[t >> 1][kb][t & 1]), a);
+        }
+      };
+
+      load_nd(0);
+      static_for<kOpAhead>([&](auto ic) { opq[decltype(ic)::value] = load_op(decltype(ic)::value); });
+      static_for<64>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        constexpr int f = j >> 1;
+        if constexpr ((j & 1) == 0 && f + kOpAhead < 32) opq[(f + kOpAhead) % (kOpAhead + 1)] = load_op(f + kOpAhead);
+        if constexpr (j == 6) load_nd(1);
+        // P fragment (rb, kb, tt) three slots before its first element
+        static_for<8>([&](auto fc) {
+          constexpr int fr = decltype(fc)::value;
+          constexpr int rb = fr >> 2, kb = (fr >> 1) & 1, tt = fr & 1;
+          if constexpr (b_slot(16 * (2 * rb + tt) + 8 * kb) - 3 == j) pf[rb][kb][tt] = xr[fr * 64 + lane];
+        });
+        static_for<64>([&](auto ec) {
+          constexpr int e = decltype(ec)::value;
+          if constexpr (b_slot(e) == j) element(e);
+        });
+        mfma(j, opq[f % (kOpAhead + 1)]);
+        if constexpr (j == 2) dma_piece(dm, 8);
+        if constexpr ((j & 7) == 4) dma_piece(dm, j >> 3);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    };
+
+    issue_all(2, 1);  // stage -1: the partner computes P of tile 0
+    stage_end();
+    for (int s = 0; s < ntiles; ++s) {
+      stage(sm.qs[s % kQBufs], sm.gs[s % kGBufs], &sm.x[s & 1][pair][0][0], dma_begin(s + 3, s + 2));
+      stage_end();
+    }
+    mfma_drain();
+  }
   __builtin_amdgcn_s_waitcnt(0);  // no direct load outlives the workgroup
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt) {  // the reads below stay after the last drain
-    acc_settle(dk[nt]);
-    acc_settle(dv[nt]);
-  }
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc_settle(acc[kb][nt]);  // the reads below stay after the drain
 
-  // ---- write dK (scaled) and dV: accumulator column = dim, rows = keys
-  void* dkout = p.dk_step[tile.step];
-  void* dvout = p.dv_step[tile.step];
+  // ---- write dV (score side) or dK (gradient side, scaled): accumulator
+  // column = dim, rows = keys
+  void* out = scorer ? p.dv_step[tile.step] : p.dk_step[tile.step];
+  const float mul = scorer ? 1.f : p.scale;
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt)
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int key = 32 * wave + 8 * (v >> 2) + 4 * half + (v & 3);
-      if (key < tile.nk) {
-        const int64_t idx = (key0 + key) * kv_row_stride + tile.kvh * kHeadDim + 32 * nt + qi;
-        store_grad(dkout, idx, dk[nt][v] * p.scale, p.grad_f32);
-        store_grad(dvout, idx, dv[nt][v], p.grad_f32);
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = 64 * pair + 32 * kb + 8 * (v >> 2) + 4 * half + (v & 3);
+        if (key < tile.nk) {
+          const int64_t idx = (key0 + key) * kv_row_stride + tile.kvh * kHeadDim + 32 * nt + qi;
+          store_grad(out, idx, acc[kb][nt][v] * mul, p.grad_f32);
+        }
       }
-    }
 }
 
 // ------------------------------------------------------------ dq
@@ -368,7 +589,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
   const int64_t acc_row = (int64_t)(tile.tok_begin + tl) * p.hq + head;
 
   bf16x8 qreg[8], greg[8];
-  float lse2 = 0.f, dlt = 0.f;
+  float lse2 = 0.f, ndl = 0.f;  // LSE log2 e, -Delta
   if (valid) {
     const bf16* qp = row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head);
     const bf16* gp = row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head);
@@ -379,7 +600,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
     }
     const float2 rs = p.rowstat[acc_row];
     lse2 = rs.x;
-    dlt = rs.y;
+    ndl = rs.y;
   } else {
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
@@ -423,7 +644,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
             const int u = kv0 + 32 * kt + 8 * (v >> 2) + 4 * half + (v & 3);
             pr = u < my_lim ? pr : 0.f;
           }
-          dp[kt][v] = pr * (dp[kt][v] - dlt);
+          dp[kt][v] = pr * (dp[kt][v] + ndl);
         }
       // ---- dQ^T += K^T dS^T: k-block t = keys 16t.. of the tile; the lane's
       // dS^T values of half h are keys 16t+4h+{0..3}, 16t+8+4h+{0..3}
@@ -506,7 +727,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
     pdot += xor32(pdot);
     if (!active) continue;
     const float pr = fast_exp2(sdot * p.scale_log2 - lse2);
-    const float ds = pr * (pdot - dlt);
+    const float ds = pr * (pdot + ndl);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -571,7 +792,7 @@ __global__ __launch_bounds__(256) void bwd_branch_kernel(BwdParams p) {
         pdot += __shfl_xor(pdot, m);
       }
       const float pr = fast_exp2(sdot * p.scale_log2 - rs.x);
-      const float ds = pr * (pdot - rs.y);
+      const float ds = pr * (pdot + rs.y);  // rs.y = -Delta
       atomicAdd(&acc_s[j * kHeadDim + 2 * lane], ds * q0);
       atomicAdd(&acc_s[j * kHeadDim + 2 * lane + 1], ds * q1);
       atomicAdd(&acc_s[(n + j) * kHeadDim + 2 * lane], pr * g0);

@@ -209,6 +209,20 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)(p));
 }
+// Per-lane LDS byte address, and 16-byte / transposed 8-byte reads at such
+// an address: a compile-time constant added to the address folds into the
+// instruction's offset field, so fragments at fixed distances from one base
+// cost no address arithmetic.
+__device__ __forceinline__ uint32_t lds_lane_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)(p);
+}
+__device__ __forceinline__ bf16x8 lds_ld16(uint32_t a) {
+  return *(const __attribute__((address_space(3))) bf16x8*)(uintptr_t)a;
+}
+__device__ __forceinline__ bf16x4 lds_ld_tr4(uint32_t a) {
+  const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(uintptr_t)a);
+  return __builtin_bit_cast(bf16x4, r);
+}
 
 // s_waitcnt vmcnt(N) (expcnt and lgkmcnt left alone) / vmcnt(N) lgkmcnt(0)
 template <int N>
