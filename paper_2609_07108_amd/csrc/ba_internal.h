@@ -114,7 +114,7 @@ struct WorkspaceLayout {
   size_t tables = 0;   // start of the table image
   size_t o_acc = 0;    // fp32 [T, hq, d]   (per-step forward)
   size_t lse_acc = 0;  // fp32 [T, hq]      (per-step forward)
-  size_t rowstat = 0;  // float2 [T, hq]    (backward: LSE*log2e, -Delta)
+  size_t rowstat = 0;  // float2 [T, hq]    (backward: -LSE*log2e, -Delta)
   size_t qtok = 0;     // bf16 [T, hq, d]   (backward: Q in token order)
   size_t gtok = 0;     // bf16 [T, hq, d]   (backward: dO in token order)
   size_t dq_acc = 0;   // fp32 [T, hq, d]   (backward)

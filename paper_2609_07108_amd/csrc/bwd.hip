@@ -9,7 +9,7 @@
 //   dK += scale dS^T Q,  dQ += scale dS K.
 //
 // Kernels
-//   preprocess : Delta and LSE * log2(e) per (query token, head).
+//   preprocess : -Delta and -LSE * log2(e) per (query token, head).
 //   kv         : dK and dV.  One workgroup per 128 keys of one ring-step
 //                block, sequence and KV head, as two wavefront pairs of 64
 //                keys (one wavefront of a pair computes P and dV, the other
@@ -48,9 +48,9 @@ __device__ __forceinline__ void store_grad(void* base, int64_t idx, float v, boo
 }  // namespace
 
 // ------------------------------------------------------------ preprocess
-// 32 lanes per (token, head): -Delta = -<dO, O> over 128 dims and the row's
-// LSE in log2 units (Delta is stored negated so the dK/dV kernel can start
-// its dP accumulation from it); Q and dO rows are also copied into token order, so the
+// 32 lanes per (token, head): -Delta = -<dO, O> over 128 dims and -LSE in
+// log2 units (both stored negated so the dK/dV kernel can start its S and dP
+// accumulations from them); Q and dO rows are also copied into token order, so the
 // dK/dV kernel addresses a query tile without indirection.
 __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
   const int64_t pair = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 5;
@@ -73,7 +73,7 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
   if (sub == 0) {
     const float lse = tk.qrow >= 0 ? p.lse_main[(int64_t)head * p.n_local + tk.qrow]
                                    : p.lse_br[(int64_t)head * p.n_br + (-tk.qrow - 1)];
-    p.rowstat[pair] = make_float2(lse * kLog2e, -dlt);
+    p.rowstat[pair] = make_float2(-lse * kLog2e, -dlt);
   }
 }
 
@@ -81,10 +81,12 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
 // Workgroup of 4 wavefronts (one per SIMD, up to 512 registers each) on 128
 // keys, as two wavefront pairs of 64 keys: pair p owns keys 64p..64p+63.
 // Inside a pair the work of the four contractions is split by operand:
-//   score wavefront (w = p):     K of the pair's keys in registers;
-//                                S = Q K^T, P = exp2(S scale log2e - LSE
-//                                log2e) with the causal mask, P handed to
-//                                the partner through LDS, dV += P^T dO
+//   score wavefront (w = p):     K scale log2e of the pair's keys in
+//                                registers; S' = Q (K scale log2e)^T - LSE
+//                                log2e (the accumulation starts from -LSE
+//                                log2e), P = exp2(S') with the causal mask,
+//                                P handed to the partner through LDS,
+//                                dV += P^T dO
 //   gradient wavefront (w = 2+p): V in registers; dP - Delta = dO V^T -
 //                                Delta (the accumulation starts from
 //                                -Delta), dS = P o (dP - Delta) with P read
@@ -118,7 +120,7 @@ constexpr int kGBufs = 3;
 
 struct QSide {
   bf16 q[kBwdRows * kHeadDim];
-  float l2[kBwdRows];  // LSE * log2 e
+  float l2[kBwdRows];  // -LSE * log2 e
   int pl[kBwdRows];    // causal limit P (-1: no token)
 };
 struct GSide {
@@ -301,13 +303,21 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   const bf16* kvsrc = (scorer ? p.k_step[tile.step] : p.v_step[tile.step]) + tile.kvh * kHeadDim;
 
   if (scorer) {
-    // K of the lane's keys (B operands of S = Q K^T), resident in the
-    // accumulation registers
+    // K scale log2e of the lane's keys (B operands of S'), resident in the
+    // accumulation registers.  Rounding the scaled K to bf16 perturbs each
+    // score by about 2^-9 of |q| |k| scale (relative), well inside the
+    // gradients' tolerance, and saves one multiply-add per probability.
     bf16x8 kreg[2][8];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int c = 0; c < 8; ++c) load16_agpr(kreg[kb][c], kvsrc + (key0 + kload[kb]) * kv_row_stride + 16 * c + 8 * half);
+      for (int c = 0; c < 8; ++c) {
+        const bf16x8 kr = ld16(kvsrc + (key0 + kload[kb]) * kv_row_stride + 16 * c + 8 * half);
+        bf16x8 ks;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ks[e] = (bf16)((float)kr[e] * p.scale_log2);
+        asm volatile("" : "=a"(kreg[kb][c]) : "0"(ks));
+      }
     zero_acc();
     __builtin_amdgcn_s_waitcnt(0);
     lds_barrier();
@@ -325,9 +335,8 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
       constexpr bool NEXT = decltype(next_tag)::value;
       constexpr bool CUR = decltype(cur_tag)::value;
       constexpr int f_lo = NEXT ? 0 : 16, f_hi = CUR ? 32 : 16;
-      f32x16 s[2][2];
+      f32x16 s[2][2], nl[2];
       bf16x8 opq[kOpAhead + 1];
-      float4 sl[2][4];
       int4 sp[2][4];
       float prv = 0.f;
 
@@ -337,17 +346,24 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
         // rows 16t+4h+{0..3}, 16t+8+4h+{0..3}: the rows of the lane's P values
         return tr_frag(ob, (f - 16) >> 2, (f - 16) & 3);
       };
-      auto load_stats = [&](int rb, int q) {
-        const int r0 = 32 * rb + 8 * q + 4 * half;
-        sl[rb][q] = *reinterpret_cast<const float4*>(&qn.l2[r0]);
-        if (MASK) sp[rb][q] = *reinterpret_cast<const int4*>(&qn.pl[r0]);
+      auto load_nl = [&](int rb) {  // -LSE log2e of the accumulator rows of row block rb
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 l4 = *reinterpret_cast<const float4*>(&qn.l2[32 * rb + 8 * q + 4 * half]);
+          nl[rb][4 * q] = l4.x;
+          nl[rb][4 * q + 1] = l4.y;
+          nl[rb][4 * q + 2] = l4.z;
+          nl[rb][4 * q + 3] = l4.w;
+        }
+      };
+      auto load_lim = [&](int rb, int q) {
+        sp[rb][q] = *reinterpret_cast<const int4*>(&qn.pl[32 * rb + 8 * q + 4 * half]);
       };
       // element e: rb = e/32, q = (e/8)%4, kb = (e/4)%2, accumulator slot
       // v = 4q + e%4 (row 32 rb + 8q + 4h + e%4)
       auto element = [&](int e) {
         const int rb = e >> 5, q = (e >> 3) & 3, kb = (e >> 2) & 1, c = e & 3, v = 4 * q + c;
-        const float l = c == 0 ? sl[rb][q].x : c == 1 ? sl[rb][q].y : c == 2 ? sl[rb][q].z : sl[rb][q].w;
-        float pr = fast_exp2(__builtin_fmaf(s[rb][kb][v], p.scale_log2, -l));
+        float pr = fast_exp2(s[rb][kb][v]);
         if (MASK) {
           const int lim = c == 0 ? sp[rb][q].x : c == 1 ? sp[rb][q].y : c == 2 ? sp[rb][q].z : sp[rb][q].w;
           pr = kpos[kb] <= lim ? pr : 0.f;
@@ -358,7 +374,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
       auto mfma = [&](int j, const bf16x8& a) {
         if (j < 32) {
           const int rb = j >> 4, c = (j >> 1) & 7, kb = j & 1;
-          if (c == 0) mfma32_v_first(s[rb][kb], a, kreg[kb][c]);
+          if (c == 0) mfma32_v_init(s[rb][kb], a, kreg[kb][0], nl[rb]);
           else mfma32_v(s[rb][kb], a, kreg[kb][c]);
         } else {
           const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3, kb = jj & 1;
@@ -366,6 +382,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
         }
       };
 
+      if constexpr (NEXT) load_nl(0);
       static_for<kOpAhead>([&](auto ic) {
         constexpr int f = f_lo + decltype(ic)::value;
         if constexpr (f < f_hi) opq[f % (kOpAhead + 1)] = load_op(f);
@@ -377,11 +394,14 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
         if constexpr (active && (j & 1) == 0 && f + kOpAhead < f_hi)
           opq[(f + kOpAhead) % (kOpAhead + 1)] = load_op(f + kOpAhead);
         if constexpr (NEXT) {
-          // statistics of rows 32 rb + 8 q + 4h.. three slots before their elements
-          static_for<8>([&](auto gc_) {
-            constexpr int g = decltype(gc_)::value;
-            if constexpr (a_slot(8 * g) - 3 == j) load_stats(g >> 2, g & 3);
-          });
+          if constexpr (j == 6) load_nl(1);
+          // causal limits of rows 32 rb + 8 q + 4h.. three slots before their elements
+          if constexpr (MASK) {
+            static_for<8>([&](auto gc_) {
+              constexpr int g = decltype(gc_)::value;
+              if constexpr (a_slot(8 * g) - 3 == j) load_lim(g >> 2, g & 3);
+            });
+          }
           static_for<64>([&](auto ec) {
             constexpr int e = decltype(ec)::value;
             if constexpr (a_slot(e) == j) element(e);
@@ -589,7 +609,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
   const int64_t acc_row = (int64_t)(tile.tok_begin + tl) * p.hq + head;
 
   bf16x8 qreg[8], greg[8];
-  float lse2 = 0.f, ndl = 0.f;  // LSE log2 e, -Delta
+  float nl2 = 0.f, ndl = 0.f;  // -LSE log2 e, -Delta
   if (valid) {
     const bf16* qp = row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head);
     const bf16* gp = row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head);
@@ -599,7 +619,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
       greg[c] = ld16(gp + 16 * c + 8 * half);
     }
     const float2 rs = p.rowstat[acc_row];
-    lse2 = rs.x;
+    nl2 = rs.x;
     ndl = rs.y;
   } else {
 #pragma unroll
@@ -639,7 +659,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          float pr = fast_exp2(__builtin_fmaf(s[kt][v], p.scale_log2, -lse2));
+          float pr = fast_exp2(__builtin_fmaf(s[kt][v], p.scale_log2, nl2));
           if (MASK) {
             const int u = kv0 + 32 * kt + 8 * (v >> 2) + 4 * half + (v & 3);
             pr = u < my_lim ? pr : 0.f;
@@ -726,7 +746,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
     sdot += xor32(sdot);
     pdot += xor32(pdot);
     if (!active) continue;
-    const float pr = fast_exp2(sdot * p.scale_log2 - lse2);
+    const float pr = fast_exp2(sdot * p.scale_log2 + nl2);
     const float ds = pr * (pdot + ndl);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
@@ -791,7 +811,7 @@ __global__ __launch_bounds__(256) void bwd_branch_kernel(BwdParams p) {
         sdot += __shfl_xor(sdot, m);
         pdot += __shfl_xor(pdot, m);
       }
-      const float pr = fast_exp2(sdot * p.scale_log2 - rs.x);
+      const float pr = fast_exp2(sdot * p.scale_log2 + rs.x);  // rs.x = -LSE log2 e
       const float ds = pr * (pdot + rs.y);  // rs.y = -Delta
       atomicAdd(&acc_s[j * kHeadDim + 2 * lane], ds * q0);
       atomicAdd(&acc_s[j * kHeadDim + 2 * lane + 1], ds * q1);

@@ -50,6 +50,11 @@ __device__ __forceinline__ void mfma32_v_first(f32x16& d, const bf16x8& a, const
 __device__ __forceinline__ void mfma32_v(f32x16& d, const bf16x8& a, const bf16x8& b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "a"(b));
 }
+// mfma32_v_first with the accumulation starting from c (vector registers);
+// s_nop 1 pads an addend just written by a vector instruction.
+__device__ __forceinline__ void mfma32_v_init(f32x16& d, const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
+}
 
 // 16-byte global load straight into accumulation registers (for MFMA
 // operands that stay resident there).  Untracked by the compiler: the caller

@@ -73,7 +73,7 @@ struct BwdParams {
   void* dk_br;
   void* dv_br;
   int32_t grad_f32;
-  float2* rowstat;  // [T * hq]: (LSE * log2 e, -Delta = -<dO, O>)
+  float2* rowstat;  // [T * hq]: (-LSE * log2 e, -Delta = -<dO, O>)
   bf16* qtok;       // [T * hq, d] Q rows in token order (written by the preprocess)
   bf16* gtok;       // [T * hq, d] dO rows in token order
   float* dq_acc;    // [T * hq, d] running unscaled dS K sums (per-step schedule)
