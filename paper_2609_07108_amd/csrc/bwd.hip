@@ -378,7 +378,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
           else mfma32_v(s[rb][kb], a, kreg[kb][c]);
         } else {
           const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3, kb = jj & 1;
-          mfma32_acc(acc[kb][nt], __builtin_bit_cast(bf16x8, pc[t >> 1][kb][t & 1]), a);
+          mfma32_acc<false>(acc[kb][nt], __builtin_bit_cast(bf16x8, pc[t >> 1][kb][t & 1]), a);  // P from the last stage
         }
       };
 
@@ -515,7 +515,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
           dp[rb][kb] = mfma32(a, vreg[kb][c], c ? dp[rb][kb] : nd[rb]);
         } else {
           const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3, kb = jj & 1;
-          mfma32_acc(acc[kb][nt], __builtin_bit_cast(bf16x8, dsf[t >> 1][kb][t & 1]), a);
+          mfma32_acc<false>(acc[kb][nt], __builtin_bit_cast(bf16x8, dsf[t >> 1][kb][t & 1]), a);  // dS >= 2 slots ago
         }
       };
 

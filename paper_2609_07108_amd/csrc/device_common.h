@@ -32,12 +32,17 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
 // then keeps them there instead of moving them between register files.  It
 // does not see this as an MFMA, so the caller guarantees the hazards it
 // would otherwise pad: the A/B operands are not written by a VALU
-// instruction just before (two wait states are padded), no other MFMA
-// writes the accumulator within the latency of this one, and mfma_drain()
-// separates the last one from any VALU read or move of the accumulator.
+// instruction within two wait states (kPad pads them with s_nop 1; callers
+// whose schedule keeps the producing instruction slots away pass false, and
+// the generated code is checked for it), no other MFMA writes the
+// accumulator within the latency of this one, and mfma_drain() separates
+// the last one from any VALU read or move of the accumulator.
+template <bool kPad = true>
 __device__ __forceinline__ void mfma32_acc(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  // s_nop 1: two wait states for an operand just written by a VALU instruction
-  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+  if constexpr (kPad)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+  else
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
 // MFMA with a vector-register accumulator and the B operand held in the
 // accumulation registers (so long-lived B operands do not occupy vector

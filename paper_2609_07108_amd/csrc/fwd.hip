@@ -92,10 +92,16 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
   f32x16 o[2][4];  // O^T accumulators, d = 32 dt + 8 (v/4) + 4 half + v%4
   float m_use[2] = {-INFINITY, -INFINITY};  // reference maximum of the exponentials (log2)
   float lsum[2] = {0.f, 0.f};               // this lane's share of the row sum
+  if constexpr (MODE == kModeFinal) {
+    // no ring walk: no MFMA ever accumulates into O here
+    for (int rb = 0; rb < 2; ++rb)
+      for (int dt = 0; dt < 4; ++dt) o[rb][dt] = f32x16{};
+  } else {
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+    for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(o[rb][dt]);
+      for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(o[rb][dt]);
+  }
 
   const int Pmin = p.toks[tile.tok_begin].P;
   const int Pmax = p.toks[tile.tok_begin + tile.ntok - 1].P;
@@ -182,7 +188,10 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
                        const float (&m_eff)[2], float (&mx_n)[2], auto&& issue_piece) {
       typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
       bf16x8 fq[kFragAhead + 1];
-      bf16x2 pk[2][4][4];  // packed P^T: [row block][t4][pair]
+      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+      // packed P^T as bf16 pairs, converted in the element's own slot:
+      // [row block][t4] -> the B operand of the t4-th O^T MFMA
+      u32x4 pk[2][4];
       float pv[2][4][8];
       auto frag = [&](int f) -> bf16x8 { return f < 16 ? s_frag(ks_n, f) : v_frag(vs_c, f - 16); };
       auto element = [&](int e) {
@@ -191,11 +200,10 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
         const float pr = fast_exp2(__builtin_fmaf(x, p.scale_log2, -m_eff[rb]));
         pv[rb][t4][i] = pr;
         lsum[rb] += pr;  // fp32 probabilities: the LSE bar is tighter than bf16 rounding
-        if (i & 1) pk[rb][t4][i >> 1] = bf16x2{(bf16)pv[rb][t4][i - 1], (bf16)pr};
+        if (i & 1) pk[rb][t4][i >> 1] = __builtin_bit_cast(uint32_t, bf16x2{(bf16)pv[rb][t4][i - 1], (bf16)pr});
       };
       auto pa = [&](int rb, int t4) {
-        return bf16x8{pk[rb][t4][0][0], pk[rb][t4][0][1], pk[rb][t4][1][0], pk[rb][t4][1][1],
-                      pk[rb][t4][2][0], pk[rb][t4][2][1], pk[rb][t4][3][0], pk[rb][t4][3][1]};
+        return __builtin_bit_cast(bf16x8, pk[rb][t4]);
       };
       static_for<kFragAhead>([&](auto fc) { fq[fc.value] = frag(fc.value); });
       static_for<64>([&](auto jc) {
@@ -210,7 +218,7 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
           s_mfma(Sn, f, rb, fq[f % (kFragAhead + 1)]);
         } else {
           constexpr int g = f - 16, t4 = g >> 2, dt = g & 3;
-          mfma32_acc(o[rb][dt], fq[f % (kFragAhead + 1)], pa(rb, t4));
+          mfma32_acc<false>(o[rb][dt], fq[f % (kFragAhead + 1)], pa(rb, t4));  // P^T packed >= 5 slots ago
         }
         if constexpr (j == 63) tile_max(Sn, mx_n);
         if constexpr ((j & 7) == 4) issue_piece(j >> 3);  // direct loads of tile t+2, spread out
