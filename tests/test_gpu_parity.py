@@ -2,7 +2,9 @@
 same seeded bf16 inputs, element by element.
 
 The cases span several query and key tiles with ragged tails, every GQA
-ratio the kernels tile differently (G = 1, 4, 8, 16), both branch kinds,
+ratio the kernels tile differently (G = 1, 2, 4, 8, 16, the maximum 64, and
+G = 3, which leaves rows of every 64- and 256-row tile without a token),
+both branch kinds,
 both branch-array layouts, both ring schedules, context-parallel ranks at
 either end of the ring, an empty sequence, sequences without branches, fp32
 gradient output, all-equal scores (Q = 0), and the mask variants of the
@@ -49,6 +51,12 @@ def case(name):
                                               ("eagle", 64)],
                         hq=16, hkv=4, cp_size=2, cp_rank=1, seed=207, has_main=[True, False, True, True],
                         name=name)
+    if name == "gqa_g3":
+        return W.custom([640, 384], [("eagle", 4), ("dflash", 16, 64)], hq=12, hkv=4, cp_size=2, cp_rank=0,
+                        seed=208, name=name)
+    if name == "gqa_g64":
+        return W.custom([512, 256], [("eagle", 2), None], hq=64, hkv=1, cp_size=2, cp_rank=1, seed=209,
+                        name=name)
     raise KeyError(name)
 
 
@@ -79,6 +87,8 @@ def test_config1_forward_every_rank(cuda, mode, r):
     ("mixed_g16", "depth", torch.bfloat16),
     ("edge_g1", "group", torch.float32),
     ("mask_variants", "depth", torch.bfloat16),
+    ("gqa_g3", "group", torch.bfloat16),
+    ("gqa_g64", "depth", torch.float32),
 ])
 def test_forward_backward_parity(cuda, mode, name, layout, grad_dtype):
     prob = case(name)
