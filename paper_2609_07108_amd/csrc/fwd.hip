@@ -128,22 +128,36 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     constexpr uint32_t kTileBytes = kFwdKeys * kHeadDim * sizeof(bf16);
     const uint32_t kv_lds = lds_addr(&kvbuf[0][0][0]);
     // direct loads of tile c into buffer buf: 16 per tensor, 4 per
-    // wavefront; piece k = 2 m4 + tensor of this wavefront's eight
-    auto fetch_piece = [&](const KvCursor& c, int buf, int k) {
-      const int m4 = k >> 1, tensor = k & 1;
+    // wavefront; piece k = 2 m4 + tensor of this wavefront's eight.  The
+    // scalar part is computed once per tile and the K and V row bases are
+    // pinned in scalar registers: re-reading the ring block's pointer from
+    // the kernel arguments per piece would wait on the scalar load, and
+    // that wait also drains the LDS operand reads in flight.
+    struct DmaTile {
+      const void* kb;
+      const void* vb;
+      uint32_t dst;
+      int nrow;  // rows past the visible prefix repeat its last row
+    };
+    auto dma_tile = [&](const KvCursor& c, int buf) {
       const int64_t row0 = ((int64_t)seq.seg_off + c.kv0) * kv_row_stride + tile.kvh * kHeadDim;
-      const void* base = uniform_ptr((tensor ? p.v_step[c.j] : p.k_step[c.j]) + row0);
-      const uint32_t dst = kv_lds + (uint32_t)(2 * buf + tensor) * kTileBytes;
-      const int nrow = c.lim_hi - c.kv0;  // rows past the visible prefix repeat its last row
+      DmaTile d{uniform_ptr(p.k_step[c.j] + row0), uniform_ptr(p.v_step[c.j] + row0),
+                kv_lds + (uint32_t)(2 * buf) * kTileBytes, c.lim_hi - c.kv0};
+      asm volatile("" : "+s"(d.kb), "+s"(d.vb));
+      return d;
+    };
+    auto fetch_piece = [&](const DmaTile& d, int k) {
+      const int m4 = k >> 1, tensor = k & 1;
       const int m = 4 * wave + m4;
       int u = dma_row<kFwdKeys>(m, lane);
-      u = u < nrow ? u : nrow - 1;
+      u = u < d.nrow ? u : d.nrow - 1;
       const uint32_t off = (uint32_t)(u * (int)kv_row_stride + dma_col<kFwdKeys>(m, lane)) * 2u;
-      dma16_async(base, off, dst + dma_dst_bytes<kFwdKeys>(m));
+      dma16_async(tensor ? d.vb : d.kb, off, d.dst + (uint32_t)tensor * kTileBytes + dma_dst_bytes<kFwdKeys>(m));
     };
     auto fetch = [&](const KvCursor& c, int buf) {
+      const DmaTile d = dma_tile(c, buf);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) fetch_piece(c, buf, k);
+      for (int k = 0; k < 8; ++k) fetch_piece(d, k);
     };
 
     // ---- S^T of a tile: fragment f = 8 kb + c (keys 32 kb.., dims 16 c..)
@@ -293,12 +307,12 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
         const KvCursor n2 = next(nxt);
         // with no tile t+2 the loads repeat tile t into the idle buffer
         const KvCursor ld = n2.i < step_end ? n2 : cur;
-        const int b2 = (t + 2) % kKvBufs;
+        const DmaTile d2 = dma_tile(ld, (t + 2) % kKvBufs);
         if (cur.kv0 + kFwdKeys > visible_keys(Pmin, cur.j, p.C, seq.c)) mask_tile(Sc, cur, mx);
         update_max(mx, m_eff);
         // with no tile t+1 the S^T MFMAs read a stale buffer and are discarded
         iterate(Sc, Sn, &kvbuf[(t + 1) % kKvBufs][0][0], &kvbuf[t % kKvBufs][1][0], m_eff, mx,
-                [&](int k) { fetch_piece(ld, b2, k); });
+                [&](int k) { fetch_piece(d2, k); });
         wait_vmcnt_lgkm0<0>();  // tile t+2 has landed for this wavefront
         lds_barrier();
         cur = nxt;
