@@ -33,13 +33,13 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/clk x 2.4 GHz
 
 # HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE runs of
-# this benchmark (256K headline share, fused schedule), scaled by a plain-copy
+# this benchmark (256K headline share, per-step schedule), scaled by a plain-copy
 # calibration (profiles/traffic_eagle3-K3-L262144-cp8r0.md).  A figure only
 # applies while the kernel's source is the one that was measured.
 MEASURED_TRAFFIC = {
-    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "e63980113a06671f", "bytes": 34734704529},
-    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "e63980113a06671f", "bytes": 14991758760},
-    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "fed3ba8aec22a72b", "bytes": 14552419957},
+    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "f153dabc1e8c0405", "bytes": 34174919390},
+    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "f153dabc1e8c0405", "bytes": 15022783303},
+    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "ebcd3a67e371a5e2", "bytes": 7822587899},
 }
 
 def measured_traffic(kernel: str, workload: str, mode: str):
