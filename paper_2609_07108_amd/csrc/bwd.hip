@@ -17,9 +17,11 @@
 //                tokens that reach those keys in 64-row tiles (tokens x the
 //                G heads of the KV head), prefetched into LDS by direct
 //                global-to-LDS loads.  No atomics.
-//   dq         : dQ, query-tile parallel like the forward: per key tile
-//                S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T, with the
-//                branch-local keys handled in the epilogue.  Splitting dQ off
+//   dq         : dQ, query-tile parallel like the forward (256-row tiles,
+//                64 rows per wavefront): per key tile S^T = K Q^T,
+//                dP^T = V dO^T, dS^T, dQ^T += K^T dS^T, software-pipelined
+//                across key tiles, with the branch-local keys handled in the
+//                epilogue.  Splitting dQ off
 //                costs two extra contractions but avoids fp32 atomics, whose
 //                throughput (about one 4-byte update per L2 channel and clock)
 //                would otherwise bound the whole backward.
@@ -43,6 +45,44 @@ __device__ __forceinline__ const bf16* row_ptr(const bf16* main, const bf16* br,
 __device__ __forceinline__ void store_grad(void* base, int64_t idx, float v, bool f32) {
   if (f32) static_cast<float*>(base)[idx] = v;
   else static_cast<bf16*>(base)[idx] = (bf16)v;
+}
+
+// Operand fragments of a 64-row plane tile sit at compile-time offsets from
+// four per-lane bases: row fragments (rows 32 rb + qi, columns 16 c + 8h;
+// the chunk permutation depends on c only through its parity) from
+// row_even / row_odd, transposed fragments (rows 16 t + 4h + {0..3} and
+// 16 t + 8 + 4h + {0..3}, columns 32 nt + ..) from tr_lo / tr_hi.  A
+// tile's bases (LDS byte addresses) are made opaque to the compiler, which
+// would otherwise re-associate the constant offsets into one register per
+// fragment.
+constexpr int kOpRows = 64;
+static_assert(kBwdRows == kOpRows && kFwdKeys == kOpRows, "operand tiles are 64 rows");
+struct LaneOffsets {
+  int row_even, row_odd, tr_lo, tr_hi;
+};
+__device__ __forceinline__ LaneOffsets lane_offsets(int lane) {
+  const int qi = lane & 31, half = lane >> 5, trc = (lane & 16) + 4 * (lane & 3);
+  return LaneOffsets{tile_off<kOpRows>(qi, 8 * half), tile_off<kOpRows>(qi, 16 + 8 * half),
+                     tile_off<kOpRows>(4 * half + ((lane & 15) >> 2), trc),
+                     tile_off<kOpRows>(8 + 4 * half + ((lane & 15) >> 2), trc)};
+}
+struct OpBases {
+  uint32_t re, ro, tl, th;
+};
+// row fragments of rowT, transposed fragments of trT
+__device__ __forceinline__ OpBases op_bases(const LaneOffsets& l, const bf16* rowT, const bf16* trT) {
+  OpBases o{lds_lane_addr(rowT + l.row_even), lds_lane_addr(rowT + l.row_odd), lds_lane_addr(trT + l.tr_lo),
+            lds_lane_addr(trT + l.tr_hi)};
+  asm volatile("" : "+v"(o.re), "+v"(o.ro), "+v"(o.tl), "+v"(o.th));
+  return o;
+}
+__device__ __forceinline__ bf16x8 row_frag(const OpBases& o, int rb, int c) {
+  return lds_ld16(((c & 1) ? o.ro : o.re) + (uint32_t)(((c >> 1) * kOpRows + 32 * rb) * 64));
+}
+__device__ __forceinline__ bf16x8 tr_frag(const OpBases& o, int t, int nt) {
+  const uint32_t off = (uint32_t)((nt * kOpRows + 16 * t) * 64);
+  const bf16x4 lo = lds_ld_tr4(o.tl + off), hi = lds_ld_tr4(o.th + off);
+  return bf16x8(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 }  // namespace
@@ -252,35 +292,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
     lds_barrier();
   };
 
-  // Operand fragments of a 64-row plane tile sit at compile-time offsets
-  // from four per-lane bases: row fragments (rows 32 rb + qi, columns
-  // 16 c + 8h; the chunk permutation depends on c only through its parity)
-  // from row_even / row_odd, transposed fragments (rows 16 t + 4h + {0..3}
-  // and 16 t + 8 + 4h + {0..3}, columns 32 nt + ..) from tr_lo / tr_hi.
-  const int row_even = tile_off<kBwdRows>(qi, 8 * half);
-  const int row_odd = tile_off<kBwdRows>(qi, 16 + 8 * half);
-  const int trc = (lane & 16) + 4 * (lane & 3);
-  const int tr_lo = tile_off<kBwdRows>(4 * half + ((lane & 15) >> 2), trc);
-  const int tr_hi = tile_off<kBwdRows>(8 + 4 * half + ((lane & 15) >> 2), trc);
-  // A stage's four bases (LDS byte addresses) are opaque to the compiler, so
-  // it cannot re-associate the constant offsets into per-fragment registers.
-  struct OpBases {
-    uint32_t re, ro, tl, th;
-  };
-  auto op_bases = [&](const bf16* rowT, const bf16* trT) __attribute__((always_inline)) {
-    OpBases o{lds_lane_addr(rowT + row_even), lds_lane_addr(rowT + row_odd), lds_lane_addr(trT + tr_lo),
-              lds_lane_addr(trT + tr_hi)};
-    asm volatile("" : "+v"(o.re), "+v"(o.ro), "+v"(o.tl), "+v"(o.th));
-    return o;
-  };
-  auto row_frag = [&](const OpBases& o, int rb, int c) __attribute__((always_inline)) {
-    return lds_ld16(((c & 1) ? o.ro : o.re) + (uint32_t)(((c >> 1) * kBwdRows + 32 * rb) * 64));
-  };
-  auto tr_frag = [&](const OpBases& o, int t, int nt) __attribute__((always_inline)) {
-    const uint32_t off = (uint32_t)((nt * kBwdRows + 16 * t) * 64);
-    const bf16x4 lo = lds_ld_tr4(o.tl + off), hi = lds_ld_tr4(o.th + off);
-    return bf16x8(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-  };
+  const LaneOffsets lo = lane_offsets(lane);
 
   // Tiles [t_lo, t_hi) need no mask: every row has a token and sees all
   // keys of the block (tokens from q_full on do).
@@ -340,7 +352,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
       int4 sp[2][4];
       float prv = 0.f;
 
-      const OpBases ob = op_bases(qn.q, gc.g);
+      const OpBases ob = op_bases(lo, qn.q, gc.g);
       auto load_op = [&](int f) -> bf16x8 {
         if (f < 16) return row_frag(ob, f >> 3, f & 7);
         // rows 16t+4h+{0..3}, 16t+8+4h+{0..3}: the rows of the lane's P values
@@ -488,7 +500,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
       u32x4 dsf[2][2][2];  // dS as bf16 pairs, the A operands of dK: [rb][kb][tt]
       float dsv = 0.f;
 
-      const OpBases ob = op_bases(gc.g, qc.q);
+      const OpBases ob = op_bases(lo, gc.g, qc.q);
       auto load_op = [&](int f) -> bf16x8 {
         if (f < 16) return row_frag(ob, f >> 3, f & 7);
         return tr_frag(ob, (f - 16) >> 2, (f - 16) & 3);
@@ -576,202 +588,421 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------ dq
-// Half a forward query tile, 128 rows (4 wavefronts x 32), per workgroup.
+// One workgroup (4 wavefronts, one per SIMD) per 256-row query tile, as in
+// the forward: wavefront w holds rows 64w.. as two 32-row blocks (rb), with
+// Q^T and dO^T of its rows (the B operands) and its dQ^T accumulators in the
+// accumulation registers.  Per 64-key tile (key blocks kb of 32 keys):
+//   S^T = K Q^T, dP^T = V dO^T   (every K or V fragment feeds both row blocks)
+//   dS^T = P^T o (dP^T - Delta), P^T = exp2(S^T scale log2e - LSE log2e)
+//   dQ^T += K^T dS^T            (every K^T fragment feeds both row blocks)
+// The 96 MFMAs of a tile run in six phases of 16 slots,
+//   S kb0 | dQ from keys 32..63 of the previous tile | dP kb0 | S kb1 |
+//   dP kb1 | dQ from keys 0..31
+// with the dS elements of key block 0 computed in the slots of S kb1 and
+// dP kb1 and those of key block 1 at the start of the next tile, so the
+// vector work runs under the matrix work without a second set of score
+// registers.  K/V tiles rotate through three LDS buffers: the previous
+// tile's K is still read in the second phase while the next tile arrives.
+// The walk runs one loop body: before the first tile a previous tile with
+// scores -inf (zero dS) stands in; after the last tile a tail iteration
+// runs only the last tile's key block 1 (no MFMA result is left unread,
+// whose registers the compiler could reuse while the MFMA still runs).
 // Accumulator layout: dQ^T, lane = one query row, rows = dims
 // 32*dt + 8*(v/4) + 4*half + v%4.
-template <int MODE>
-__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p) {
-  // [buffer][K, V] plane tiles of 64 keys (see tile_off), double-buffered
-  __shared__ __attribute__((aligned(16))) bf16 kvbuf[2][2][kFwdKeys * kHeadDim];
+namespace {
 
-  // two workgroups per query tile, rows [128 h, 128 h + 128) of it.  Block
-  // 16 g + 8 h + x takes half h of tile 8 g + x: workgroups go to the 8 XCDs
-  // round-robin by index, so both halves of a tile run on one XCD and share
-  // its L2 for the K/V tiles they both stream
-  const int qt = 8 * (blockIdx.x >> 4) + (blockIdx.x & 7);
-  if (qt >= p.num_qtiles) return;
-  const FwdTile tile = p.qtiles[qt];
-  const int rbase = 128 * ((blockIdx.x >> 3) & 1);
-  if (rbase / p.G >= tile.ntok) return;  // no token in this half
+constexpr int kDqBufs = 3;
+constexpr int kDqAhead = 2;  // operand fragments read ahead of their MFMAs (two MFMAs each)
+
+// Element e of a key block (32 per lane): the 8-key chunk tt = e/16 (keys
+// 16 tt + 8 kb.. in the lane's accumulator slots 8 tt..), row block
+// (e/8)%2, slot i = e%8.  Key block 0 of the current tile in slots
+// 54..84 (its dQ MFMAs start at 80 and 88; the last dP MFMA of key block 0
+// is in slot 47, and its result is read by a vector instruction only after
+// the 12 wait states that the compiler would pad); key block 1 of the
+// previous tile in slots 0..21 (its dQ MFMAs start at 16 and 24).
+constexpr int dq_slot0(int e) { return 54 + (e * 31) / 32; }
+constexpr int dq_slot1(int e) { return e < 16 ? e / 2 : 8 + ((e - 16) * 14) / 16; }
+
+}  // namespace
+
+template <int MODE>
+__global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
+  // [buffer][K, V] plane tiles of 64 keys (see tile_off)
+  __shared__ __attribute__((aligned(16))) bf16 kvbuf[kDqBufs][2][kFwdKeys * kHeadDim];
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+  const FwdTile tile = p.qtiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform
   const int qi = lane & 31;
   const int half = lane >> 5;
-  const int row = rbase + wave * 32 + qi;
-  const int tl = row / p.G;
-  const int head = tile.kvh * p.G + (row - tl * p.G);
-  const bool valid = tl < tile.ntok;
-  TokInfo tk;
-  if (valid) tk = p.toks[tile.tok_begin + tl];
-  else tk = TokInfo{0, -1, -1, -1};
-  const int64_t acc_row = (int64_t)(tile.tok_begin + tl) * p.hq + head;
+  const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
+  const LaneOffsets lo = lane_offsets(lane);
 
-  bf16x8 qreg[8], greg[8];
-  float nl2 = 0.f, ndl = 0.f;  // -LSE log2 e, -Delta
-  if (valid) {
-    const bf16* qp = row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head);
-    const bf16* gp = row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head);
+  // ---- the lane's two rows (row block rb: row 64 w + 32 rb + qi).  Rows
+  // without a token read the rows of the tile's last token (finite data)
+  // and take -LSE = -inf, so their probabilities and dS are zero; their dQ
+  // is never written.
+  int head[2];
+  bool valid[2];
+  TokInfo tk[2];
+  float nl2[2], ndl[2];  // -LSE log2 e, -Delta
+  bf16x8 qreg[2][8], greg[2][8];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+    const int row = 64 * wave + 32 * rb + qi;
+    const int tl = row / p.G;
+    head[rb] = tile.kvh * p.G + (row - tl * p.G);
+    valid[rb] = tl < tile.ntok;
+    tk[rb] = valid[rb] ? p.toks[tile.tok_begin + tl] : TokInfo{0, -1, -1, -1};
+    const TokInfo tq = valid[rb] ? tk[rb] : p.toks[tile.tok_begin + tile.ntok - 1];
+    const int hq_row = valid[rb] ? head[rb] : tile.kvh * p.G;
+    const bf16* qp = row_ptr(p.q_main, p.q_br, tq.qrow, p.hq, hq_row);
+    const bf16* gp = row_ptr(p.do_main, p.do_br, tq.qrow, p.hq, hq_row);
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
-      qreg[c] = ld16(qp + 16 * c + 8 * half);
-      greg[c] = ld16(gp + 16 * c + 8 * half);
+      load16_agpr(qreg[rb][c], qp + 16 * c + 8 * half);
+      load16_agpr(greg[rb][c], gp + 16 * c + 8 * half);
     }
-    const float2 rs = p.rowstat[acc_row];
-    nl2 = rs.x;
-    ndl = rs.y;
+    nl2[rb] = -INFINITY;
+    ndl[rb] = 0.f;
+    if (valid[rb]) {
+      const float2 rs = p.rowstat[(int64_t)(tile.tok_begin + tl) * p.hq + head[rb]];
+      nl2[rb] = rs.x;
+      ndl[rb] = rs.y;
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+
+  f32x16 dq[2][4];
+  if constexpr (MODE == kModeFinal) {
+    // no ring walk: no MFMA ever accumulates into dQ here
+    for (int rb = 0; rb < 2; ++rb)
+      for (int dt = 0; dt < 4; ++dt) dq[rb][dt] = f32x16{};
   } else {
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      qreg[c] = bf16x8{};
-      greg[c] = bf16x8{};
-    }
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(dq[rb][dt]);
   }
 
-  f32x16 dq[4];
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt) dq[dt] = f32x16{};
-
-  const int Pmin = p.toks[tile.tok_begin + rbase / p.G].P;
-  const int Pmax = p.toks[tile.tok_begin + min(tile.ntok - 1, (rbase + 127) / p.G)].P;
-  const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
+  const int Pmin = p.toks[tile.tok_begin].P;
+  const int Pmax = p.toks[tile.tok_begin + tile.ntok - 1].P;
 
   if (MODE != kModeFinal) {
-    // One 64-key tile: S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T.
-    // MASK (compile time) only on tiles crossing some row's causal limit.
-    auto compute = [&](int j, int kv0, const bf16* ks, const bf16* vs, auto mask_tag) {
-      constexpr bool MASK = decltype(mask_tag)::value;
-      const int my_lim = valid ? visible_keys(tk.P, j, p.C, seq.c) : 0;
-      f32x16 s[2], dp[2];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        s[kt] = f32x16{};
-        dp[kt] = f32x16{};
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          s[kt] = mfma32(ld16(&ks[tile_off<kFwdKeys>(32 * kt + qi, 16 * c + 8 * half)]), qreg[c], s[kt]);
-          dp[kt] = mfma32(ld16(&vs[tile_off<kFwdKeys>(32 * kt + qi, 16 * c + 8 * half)]), greg[c], dp[kt]);
-        }
+    // ---- cursor over (ring step, 64-key tile), as in the forward
+    const int step_end = p.step_first + p.step_count;
+    auto seek = [&](int i) {
+      KvCursor c{i, 0, 0, 0};
+      for (; c.i < step_end; ++c.i) {
+        c.j = ((p.rank - c.i) % p.C + p.C) % p.C;
+        c.lim_hi = visible_keys(Pmax, c.j, p.C, seq.c);
+        if (c.lim_hi > 0) break;
       }
-      // ---- dS^T = P^T (dP^T - Delta), P^T = exp2(S^T scale log2e - LSE log2e)
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          float pr = fast_exp2(__builtin_fmaf(s[kt][v], p.scale_log2, nl2));
-          if (MASK) {
-            const int u = kv0 + 32 * kt + 8 * (v >> 2) + 4 * half + (v & 3);
-            pr = u < my_lim ? pr : 0.f;
-          }
-          dp[kt][v] = pr * (dp[kt][v] + ndl);
-        }
-      // ---- dQ^T += K^T dS^T: k-block t = keys 16t.. of the tile; the lane's
-      // dS^T values of half h are keys 16t+4h+{0..3}, 16t+8+4h+{0..3}
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const f32x16& src = dp[t >> 1];
-        const int v0 = 8 * (t & 1);
-        const bf16x8 b = pack8(src[v0], src[v0 + 1], src[v0 + 2], src[v0 + 3], src[v0 + 4], src[v0 + 5],
-                               src[v0 + 6], src[v0 + 7]);
-        const int ka = 16 * t + 4 * half, kb = ka + 8;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma32(ld_tr8<kFwdKeys>(ks, 32 * dt, ka, kb, lane), b, dq[dt]);
+      return c;
+    };
+    auto next = [&](KvCursor c) {
+      if (c.i >= step_end) return c;
+      c.kv0 += kFwdKeys;
+      return c.kv0 < c.lim_hi ? c : seek(c.i + 1);
+    };
+    constexpr uint32_t kTileBytes = kFwdKeys * kHeadDim * sizeof(bf16);
+    const uint32_t kv_lds = lds_addr(&kvbuf[0][0][0]);
+    // direct loads of a tile: 16 per tensor, 4 per wavefront; piece k =
+    // 2 m4 + tensor.  The scalar part is computed once per tile, its row
+    // bases pinned in scalar registers.
+    struct DmaTile {
+      const void* kb;
+      const void* vb;
+      uint32_t dst;
+      int nrow;  // rows past the visible prefix repeat its last row
+    };
+    // the ring block's K/V bases, re-read from the kernel arguments only
+    // when the walk moves to another block
+    int cj = -1;
+    const bf16* ckb = nullptr;
+    const bf16* cvb = nullptr;
+    auto dma_tile = [&](const KvCursor& c, int buf) {
+      if (c.j != cj) {
+        cj = c.j;
+        ckb = p.k_step[cj];
+        cvb = p.v_step[cj];
+        asm volatile("" : "+s"(ckb), "+s"(cvb));
+      }
+      const int64_t row0 = ((int64_t)seq.seg_off + c.kv0) * kv_row_stride + tile.kvh * kHeadDim;
+      DmaTile d{uniform_ptr(ckb + row0), uniform_ptr(cvb + row0), kv_lds + (uint32_t)(2 * buf) * kTileBytes,
+                c.lim_hi - c.kv0};
+      asm volatile("" : "+s"(d.kb), "+s"(d.vb));
+      return d;
+    };
+    auto fetch_piece = [&](const DmaTile& d, int k) {
+      const int m4 = k >> 1, tensor = k & 1;
+      const int m = 4 * wave + m4;
+      int u = dma_row<kFwdKeys>(m, lane);
+      u = u < d.nrow ? u : d.nrow - 1;
+      const uint32_t off = (uint32_t)(u * (int)kv_row_stride + dma_col<kFwdKeys>(m, lane)) * 2u;
+      dma16_async(tensor ? d.vb : d.kb, off, d.dst + (uint32_t)tensor * kTileBytes + dma_dst_bytes<kFwdKeys>(m));
+    };
+
+    f32x16 s0[2], s1[2], p0[2], p1[2];  // S^T and dP^T of key blocks 0 and 1: [rb]
+    u32x4 ds0[2][2], ds1[2][2];         // dS^T as bf16 pairs: [rb][tt], B operands of dQ^T
+    float sv0 = 0.f, sv1 = 0.f;
+
+    // dS elements of a key block (scores S, dP^T accumulators P, output D)
+    auto element = [&](const f32x16 (&S)[2], const f32x16 (&P)[2], u32x4 (&D)[2][2], float& prv, int e) {
+      const int tt = e >> 4, rb = (e >> 3) & 1, i = e & 7, v = 8 * tt + i;
+      const float pr = fast_exp2(__builtin_fmaf(S[rb][v], p.scale_log2, nl2[rb]));
+      const float ds = pr * (P[rb][v] + ndl[rb]);
+      if (i & 1) {
+        uint32_t w = __builtin_bit_cast(uint32_t, bf16x2{(bf16)prv, (bf16)ds});
+        asm volatile("" : "+v"(w));  // packed in this slot, not next to the MFMA that reads it
+        D[rb][tt][i >> 1] = w;
+      } else {
+        prv = ds;
       }
     };
-    walk_kv_tiles(p, seq, tile.kvh, Pmax, wave, lane, kvbuf, [&](int j, int kv0, const bf16* ks, const bf16* vs) {
-      if (kv0 + kFwdKeys <= visible_keys(Pmin, j, p.C, seq.c)) compute(j, kv0, ks, vs, std::false_type{});
-      else compute(j, kv0, ks, vs, std::true_type{});
-    });
-  }
-
-  if (MODE == kModeStep) {
-    if (!valid) return;
-    float* dst = p.dq_acc + acc_row * kHeadDim;
+    // keys at or past a row's causal limit get score -inf (probability 0)
+    auto mask_block = [&](f32x16 (&S)[2], const KvCursor& c, int kb) {
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+      for (int rb = 0; rb < 2; ++rb) {
+        const int lim = valid[rb] ? visible_keys(tk[rb].P, c.j, p.C, seq.c) : 0;
 #pragma unroll
-      for (int vq = 0; vq < 4; ++vq) {
-        float4* d4 = reinterpret_cast<float4*>(dst + 32 * dt + 8 * vq + 4 * half);
-        float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (!p.acc_first) a = *d4;
-        a.x += dq[dt][4 * vq + 0];
-        a.y += dq[dt][4 * vq + 1];
-        a.z += dq[dt][4 * vq + 2];
-        a.w += dq[dt][4 * vq + 3];
-        *d4 = a;
-      }
-    return;
-  }
-  if (MODE == kModeFinal && valid) {
-    const float* src = p.dq_acc + acc_row * kHeadDim;
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int vq = 0; vq < 4; ++vq) {
-        const float4 a = *reinterpret_cast<const float4*>(src + 32 * dt + 8 * vq + 4 * half);
-        dq[dt][4 * vq + 0] = a.x;
-        dq[dt][4 * vq + 1] = a.y;
-        dq[dt][4 * vq + 2] = a.z;
-        dq[dt][4 * vq + 3] = a.w;
-      }
-  }
-
-  // ---- branch-local keys of this row (vector ALUs)
-  int nb = 0;
-  GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
-  if (valid && tk.grp >= 0) {
-    gi = p.groups[tk.grp];
-    nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk.gidx + 1 : gi.len;
-  }
-  for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
-    const bool active = b < nb;
-    if (__ballot(active) == 0) break;
-    const int64_t krow = (int64_t)gi.row0 + (int64_t)b * gi.stride;
-    const bf16* kb = p.k_br + krow * kv_row_stride + tile.kvh * kHeadDim;
-    const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
-    float sdot = 0.f, pdot = 0.f;
-    if (active) {
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const bf16x8 kv = ld16(kb + 16 * c + 8 * half);
-        const bf16x8 vv = ld16(vb + 16 * c + 8 * half);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          sdot += (float)qreg[c][e] * (float)kv[e];
-          pdot += (float)greg[c][e] * (float)vv[e];
+        for (int v = 0; v < 16; ++v) {
+          const int u = c.kv0 + 32 * kb + 8 * (v >> 2) + 4 * half + (v & 3);
+          if (u >= lim) S[rb][v] = -INFINITY;
         }
       }
+    };
+
+    // One tile iteration.  MFMA j (0..95): phase j/16; fragment j/2 feeds
+    // MFMAs j (row block 0) and j+1 (row block 1).  The current tile is in
+    // buffer cb, the previous one in pb; mask: apply the causal limits.
+    auto iterate = [&](auto tail_tag, int cb, int pb, const KvCursor& cur, bool mask, const DmaTile& dn,
+                       bool load_next) __attribute__((always_inline)) {
+      constexpr bool TAIL = decltype(tail_tag)::value;  // phase 1 and key block 1 of the previous tile only
+      const bf16* kc = &kvbuf[cb][0][0];
+      const bf16* vc = &kvbuf[cb][1][0];
+      const bf16* kp = &kvbuf[pb][0][0];
+      // K rows and K^T of this tile; V rows and K^T of the previous tile
+      const OpBases bk = op_bases(lo, kc, kc);
+      const OpBases bv = op_bases(lo, vc, kp);
+      auto load_op = [&](int f) -> bf16x8 {
+        const int ph = f >> 3, x = f & 7;
+        switch (ph) {
+          case 0: return row_frag(bk, 0, x);                // K keys 0..31, dims 16x..
+          case 1: return tr_frag(bv, 2 + (x >> 2), x & 3);  // K^T of the previous tile, keys 32+16(x/4)..
+          case 2: return row_frag(bv, 0, x);                // V keys 0..31
+          case 3: return row_frag(bk, 1, x);                // K keys 32..63
+          case 4: return row_frag(bv, 1, x);                // V keys 32..63
+          default: return tr_frag(bk, x >> 2, x & 3);       // K^T keys 16(x/4)..
+        }
+      };
+      auto mfma = [&](int j, const bf16x8& a) {
+        const int ph = j >> 4, jj = j & 15, x = jj >> 1, rb = jj & 1;
+        switch (ph) {
+          case 0:
+            if (x == 0) mfma32_v_first(s0[rb], a, qreg[rb][0]);
+            else mfma32_v(s0[rb], a, qreg[rb][x]);
+            break;
+          // (the tail has no MFMAs before this phase, so its dS packing can
+          // sit right before them: padded there)
+          case 1: mfma32_acc<TAIL>(dq[rb][x & 3], a, __builtin_bit_cast(bf16x8, ds1[rb][x >> 2])); break;
+          case 2:
+            if (x == 0) mfma32_v_first(p0[rb], a, greg[rb][0]);
+            else mfma32_v(p0[rb], a, greg[rb][x]);
+            break;
+          case 3:
+            if (x == 0) mfma32_v_first(s1[rb], a, qreg[rb][0]);
+            else mfma32_v(s1[rb], a, qreg[rb][x]);
+            break;
+          case 4:
+            if (x == 0) mfma32_v_first(p1[rb], a, greg[rb][0]);
+            else mfma32_v(p1[rb], a, greg[rb][x]);
+            break;
+          default: mfma32_acc<false>(dq[rb][x & 3], a, __builtin_bit_cast(bf16x8, ds0[rb][x >> 2])); break;
+        }
+      };
+      // fragments f_lo .. f_hi-1 run: all 48, or the 8 of phase 1
+      constexpr int f_lo = TAIL ? 8 : 0, f_hi = TAIL ? 16 : 48;
+      bf16x8 opq[kDqAhead + 1];  // read-ahead ring
+      static_for<kDqAhead>([&](auto fc) {
+        constexpr int f = f_lo + decltype(fc)::value;
+        opq[f % (kDqAhead + 1)] = load_op(f);
+      });
+      static_for<96>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        constexpr int f = j >> 1;
+        constexpr bool act = f >= f_lo && f < f_hi;
+        if constexpr (act && (j & 1) == 0 && f + kDqAhead < f_hi)
+          opq[(f + kDqAhead) % (kDqAhead + 1)] = load_op(f + kDqAhead);
+        static_for<32>([&](auto ec) {
+          constexpr int e = decltype(ec)::value;
+          if constexpr (dq_slot1(e) == j) element(s1, p1, ds1, sv1, e);
+        });
+        if constexpr (!TAIL) {
+          if constexpr (j == 24) {
+            if (mask) mask_block(s0, cur, 0);
+          }
+          if constexpr (j == 70) {
+            if (mask) mask_block(s1, cur, 1);
+          }
+          static_for<32>([&](auto ec) {
+            constexpr int e = decltype(ec)::value;
+            if constexpr (dq_slot0(e) == j) element(s0, p0, ds0, sv0, e);
+          });
+          if constexpr ((j & 7) == 4 && j < 64) {
+            if (load_next) fetch_piece(dn, j >> 3);
+          }
+        }
+        if constexpr (act) mfma(j, opq[f % (kDqAhead + 1)]);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    };
+
+    KvCursor cur = seek(p.step_first);
+    if (cur.i < step_end) {
+      {
+        const DmaTile d0 = dma_tile(cur, 0);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) fetch_piece(d0, k);
+      }
+      // the stand-in previous tile: scores -inf, so its dS are zero
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          s1[rb][v] = -INFINITY;
+          p1[rb][v] = 0.f;
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+      lds_barrier();
+      int t = 0;
+      while (true) {
+        const KvCursor nx = next(cur);
+        const bool more = nx.i < step_end;
+        const DmaTile dn = dma_tile(more ? nx : cur, (t + 1) % kDqBufs);
+        const bool mask = cur.kv0 + kFwdKeys > visible_keys(Pmin, cur.j, p.C, seq.c);
+        // the first tile's stand-in previous tile reads this tile's (finite) K
+        iterate(std::false_type{}, t % kDqBufs, t == 0 ? 0 : (t - 1) % kDqBufs, cur, mask, dn, more);
+        wait_vmcnt_lgkm0<0>();  // tile t+1 has landed for this wavefront
+        lds_barrier();
+        ++t;
+        if (!more) break;
+        cur = nx;
+      }
+      // key block 1 of the last tile
+      iterate(std::true_type{}, 0, (t - 1) % kDqBufs, cur, false, DmaTile{}, false);
+      mfma_drain();  // dQ^T complete before the epilogue reads it
     }
-    sdot += xor32(sdot);
-    pdot += xor32(pdot);
-    if (!active) continue;
-    const float pr = fast_exp2(sdot * p.scale_log2 + nl2);
-    const float ds = pr * (pdot + ndl);
+  }
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) acc_settle(dq[rb][dt]);
+
+  // ------------------------------------------------------------ epilogues
+  // per row block; every lane runs both so cross-lane exchanges stay uniform
+  auto finish = [&](int rb) {
+    const int tl = (64 * wave + 32 * rb + qi) / p.G;
+    const int64_t acc_row = (int64_t)(tile.tok_begin + tl) * p.hq + head[rb];
+    f32x16 st[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) st[dt] = dq[rb][dt];
+    if (MODE == kModeStep) {
+      if (!valid[rb]) return;
+      float* dst = p.dq_acc + acc_row * kHeadDim;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int vq = 0; vq < 4; ++vq) {
+          float4* d4 = reinterpret_cast<float4*>(dst + 32 * dt + 8 * vq + 4 * half);
+          float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (!p.acc_first) a = *d4;
+          a.x += st[dt][4 * vq + 0];
+          a.y += st[dt][4 * vq + 1];
+          a.z += st[dt][4 * vq + 2];
+          a.w += st[dt][4 * vq + 3];
+          *d4 = a;
+        }
+      return;
+    }
+    if (MODE == kModeFinal && valid[rb]) {
+      const float* src = p.dq_acc + acc_row * kHeadDim;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int vq = 0; vq < 4; ++vq) {
+          const float4 a = *reinterpret_cast<const float4*>(src + 32 * dt + 8 * vq + 4 * half);
+          st[dt][4 * vq + 0] = a.x;
+          st[dt][4 * vq + 1] = a.y;
+          st[dt][4 * vq + 2] = a.z;
+          st[dt][4 * vq + 3] = a.w;
+        }
+    }
+
+    // ---- branch-local keys of this row (vector ALUs)
+    int nb = 0;
+    GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
+    if (valid[rb] && tk[rb].grp >= 0) {
+      gi = p.groups[tk[rb].grp];
+      nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk[rb].gidx + 1 : gi.len;
+    }
+    for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
+      const bool active = b < nb;
+      if (__ballot(active) == 0) break;
+      const int64_t krow = (int64_t)gi.row0 + (int64_t)b * gi.stride;
+      const bf16* kb = p.k_br + krow * kv_row_stride + tile.kvh * kHeadDim;
+      const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
+      float sdot = 0.f, pdot = 0.f;
+      if (active) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const bf16x8 kv = ld16(kb + 16 * c + 8 * half);
+          const bf16x8 vv = ld16(vb + 16 * c + 8 * half);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            sdot += (float)qreg[rb][c][e] * (float)kv[e];
+            pdot += (float)greg[rb][c][e] * (float)vv[e];
+          }
+        }
+      }
+      sdot += xor32(sdot);
+      pdot += xor32(pdot);
+      if (!active) continue;
+      const float pr = fast_exp2(sdot * p.scale_log2 + nl2[rb]);
+      const float ds = pr * (pdot + ndl[rb]);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int vq = 0; vq < 4; ++vq) {
+          const bf16x4 kk = *reinterpret_cast<const bf16x4*>(kb + 32 * dt + 8 * vq + 4 * half);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) st[dt][4 * vq + c] += ds * (float)kk[c];
+        }
+    }
+    if (!valid[rb]) return;
+
+    void* out = tk[rb].qrow >= 0 ? p.dq_main : p.dq_br;
+    const int64_t orow = tk[rb].qrow >= 0 ? tk[rb].qrow : -tk[rb].qrow - 1;
+    const int64_t base = (orow * p.hq + head[rb]) * kHeadDim;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int vq = 0; vq < 4; ++vq) {
-        const bf16x4 kk = *reinterpret_cast<const bf16x4*>(kb + 32 * dt + 8 * vq + 4 * half);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) dq[dt][4 * vq + c] += ds * (float)kk[c];
+        const int64_t o = base + 32 * dt + 8 * vq + 4 * half;
+        const float a0 = st[dt][4 * vq] * p.scale, a1 = st[dt][4 * vq + 1] * p.scale;
+        const float a2 = st[dt][4 * vq + 2] * p.scale, a3 = st[dt][4 * vq + 3] * p.scale;
+        if (p.grad_f32) *reinterpret_cast<float4*>(static_cast<float*>(out) + o) = make_float4(a0, a1, a2, a3);
+        else *reinterpret_cast<bf16x4*>(static_cast<bf16*>(out) + o) = pack4(a0, a1, a2, a3);
       }
-  }
-  if (!valid) return;
-
-  void* out = tk.qrow >= 0 ? p.dq_main : p.dq_br;
-  const int64_t orow = tk.qrow >= 0 ? tk.qrow : -tk.qrow - 1;
-  const int64_t base = (orow * p.hq + head) * kHeadDim;
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-    for (int vq = 0; vq < 4; ++vq) {
-      const int64_t o = base + 32 * dt + 8 * vq + 4 * half;
-      const float a0 = dq[dt][4 * vq] * p.scale, a1 = dq[dt][4 * vq + 1] * p.scale;
-      const float a2 = dq[dt][4 * vq + 2] * p.scale, a3 = dq[dt][4 * vq + 3] * p.scale;
-      if (p.grad_f32) *reinterpret_cast<float4*>(static_cast<float*>(out) + o) = make_float4(a0, a1, a2, a3);
-      else *reinterpret_cast<bf16x4*>(static_cast<bf16*>(out) + o) = pack4(a0, a1, a2, a3);
-    }
+  };
+  finish(0);
+  finish(1);
 }
 
 // ------------------------------------------------------------ branch dK/dV
@@ -854,7 +1085,7 @@ hipError_t launch_bwd_kv(const BwdParams& p, hipStream_t stream) {
 
 hipError_t launch_bwd_dq(const BwdParams& p, int mode, hipStream_t stream) {
   if (p.num_qtiles == 0) return hipSuccess;
-  dim3 grid(16 * ((p.num_qtiles + 7) / 8)), block(256);  // see the block mapping in the kernel
+  dim3 grid(p.num_qtiles), block(256);
   if (mode == kModeStep) hipLaunchKernelGGL(bwd_dq_kernel<kModeStep>, grid, block, 0, stream, p);
   else if (mode == kModeFinal) hipLaunchKernelGGL(bwd_dq_kernel<kModeFinal>, grid, block, 0, stream, p);
   else hipLaunchKernelGGL(bwd_dq_kernel<kModeFused>, grid, block, 0, stream, p);

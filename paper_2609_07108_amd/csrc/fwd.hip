@@ -139,10 +139,21 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
       uint32_t dst;
       int nrow;  // rows past the visible prefix repeat its last row
     };
+    // the ring block's K/V bases, re-read from the kernel arguments only
+    // when the walk moves to another block
+    int cj = -1;
+    const bf16* ckb = nullptr;
+    const bf16* cvb = nullptr;
     auto dma_tile = [&](const KvCursor& c, int buf) {
+      if (c.j != cj) {
+        cj = c.j;
+        ckb = p.k_step[cj];
+        cvb = p.v_step[cj];
+        asm volatile("" : "+s"(ckb), "+s"(cvb));
+      }
       const int64_t row0 = ((int64_t)seq.seg_off + c.kv0) * kv_row_stride + tile.kvh * kHeadDim;
-      DmaTile d{uniform_ptr(p.k_step[c.j] + row0), uniform_ptr(p.v_step[c.j] + row0),
-                kv_lds + (uint32_t)(2 * buf) * kTileBytes, c.lim_hi - c.kv0};
+      DmaTile d{uniform_ptr(ckb + row0), uniform_ptr(cvb + row0), kv_lds + (uint32_t)(2 * buf) * kTileBytes,
+                c.lim_hi - c.kv0};
       asm volatile("" : "+s"(d.kb), "+s"(d.vb));
       return d;
     };
