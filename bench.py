@@ -136,7 +136,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=4, help="named workload 1..5 (4 = 256K headline)")
     ap.add_argument("--mode", choices=["fused", "per_step"], default="per_step",
                     help="per_step: one launch per ring step (the ring's schedule); fused: one walk over all blocks")
