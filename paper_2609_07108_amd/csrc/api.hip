@@ -108,6 +108,7 @@ extern "C" int branch_attn_fwd(void* stream_, const ba_plan* plan, int32_t mode,
   p.hq = P.hq;
   p.hkv = P.hkv;
   p.G = P.group;
+  p.num_tokens = (int32_t)P.toks.size();
   p.scale_log2 = P.scale * kLog2e;
   p.n_local = P.n_local;
   p.n_br = P.num_branch_rows;
@@ -143,9 +144,7 @@ extern "C" int branch_attn_fwd(void* stream_, const ba_plan* plan, int32_t mode,
     if ((e = launch_fwd(p, kModeStep, stream)) != hipSuccess) return hip_fail(e, "ring-step launch");
   }
   if ((e = record(io->ring_end, stream)) != hipSuccess) return hip_fail(e, "event record");
-  p.step_first = 0;
-  p.step_count = 0;
-  if ((e = launch_fwd(p, kModeFinal, stream)) != hipSuccess) return hip_fail(e, "branch/merge launch");
+  if ((e = launch_fwd_finalize(p, stream)) != hipSuccess) return hip_fail(e, "branch/merge launch");
   return BA_OK;
 }
 
@@ -262,9 +261,7 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
       if ((e = launch_bwd_dq(p, kModeStep, stream)) != hipSuccess) return hip_fail(e, "ring-step dQ launch");
     }
     if ((e = record(io->ring_end, stream)) != hipSuccess) return hip_fail(e, "event record");
-    p.step_first = 0;
-    p.step_count = 0;
-    if ((e = launch_bwd_dq(p, kModeFinal, stream)) != hipSuccess) return hip_fail(e, "dQ finalize launch");
+    if ((e = launch_bwd_dq_finalize(p, stream)) != hipSuccess) return hip_fail(e, "dQ finalize launch");
   }
   if (has_br) {
     if ((e = launch_bwd_branch(p, P.max_group_len, stream)) != hipSuccess) return hip_fail(e, "branch backward launch");

@@ -679,21 +679,15 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
   __builtin_amdgcn_s_waitcnt(0);
 
   f32x16 dq[2][4];
-  if constexpr (MODE == kModeFinal) {
-    // no ring walk: no MFMA ever accumulates into dQ here
-    for (int rb = 0; rb < 2; ++rb)
-      for (int dt = 0; dt < 4; ++dt) dq[rb][dt] = f32x16{};
-  } else {
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(dq[rb][dt]);
-  }
+    for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(dq[rb][dt]);
 
   const int Pmin = p.toks[tile.tok_begin].P;
   const int Pmax = p.toks[tile.tok_begin + tile.ntok - 1].P;
 
-  if (MODE != kModeFinal) {
+  {
     // ---- cursor over (ring step, 64-key tile), as in the forward
     const int step_end = p.step_first + p.step_count;
     auto seek = [&](int i) {
@@ -931,20 +925,6 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
         }
       return;
     }
-    if (MODE == kModeFinal && valid[rb]) {
-      const float* src = p.dq_acc + acc_row * kHeadDim;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int vq = 0; vq < 4; ++vq) {
-          const float4 a = *reinterpret_cast<const float4*>(src + 32 * dt + 8 * vq + 4 * half);
-          st[dt][4 * vq + 0] = a.x;
-          st[dt][4 * vq + 1] = a.y;
-          st[dt][4 * vq + 2] = a.z;
-          st[dt][4 * vq + 3] = a.w;
-        }
-    }
-
     // ---- branch-local keys of this row (vector ALUs)
     int nb = 0;
     GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
@@ -1005,58 +985,180 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
   finish(1);
 }
 
-// ------------------------------------------------------------ branch dK/dV
-// One workgroup per (group, KV head).  Each wavefront takes query rows
-// (member i, head) in turn; lanes hold two dims each and every score needs a
-// wavefront-wide reduction.  The group's dK/dV are summed in LDS (fp32) and
-// written once.
-__global__ __launch_bounds__(256) void bwd_branch_kernel(BwdParams p) {
-  extern __shared__ float acc_s[];  // [2][len][128]: dK sums, dV sums
-  const int g = blockIdx.x / p.hkv;
-  const int kvh = blockIdx.x - g * p.hkv;
-  const GroupInfo gi = p.groups[g];
-  const int n = gi.len;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int i = tid; i < 2 * n * kHeadDim; i += blockDim.x) acc_s[i] = 0.f;
-  __syncthreads();
-  const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
-  const int G = p.G;
-  for (int rr = wave; rr < n * G; rr += 4) {
-    const int i = rr / G;
-    const int head = kvh * G + (rr - i * G);
-    const int64_t brow = (int64_t)gi.row0 + (int64_t)i * gi.stride;
-    const bf16* q = p.q_br + (brow * p.hq + head) * kHeadDim;
-    const bf16* g_ = p.do_br + (brow * p.hq + head) * kHeadDim;
-    const float2 rs = p.rowstat[(int64_t)(gi.tok0 + i) * p.hq + head];
-    const float q0 = (float)q[2 * lane], q1 = (float)q[2 * lane + 1];
-    const float g0 = (float)g_[2 * lane], g1 = (float)g_[2 * lane + 1];
-    const int nk = gi.kind == BA_KIND_EAGLE_CHAIN ? i + 1 : n;
-    for (int j = 0; j < nk; ++j) {
-      const int64_t krow = (int64_t)gi.row0 + (int64_t)j * gi.stride;
-      const bf16* kp = p.k_br + krow * kv_row_stride + kvh * kHeadDim;
-      const bf16* vp = p.v_br + krow * kv_row_stride + kvh * kHeadDim;
-      float sdot = q0 * (float)kp[2 * lane] + q1 * (float)kp[2 * lane + 1];
-      float pdot = g0 * (float)vp[2 * lane] + g1 * (float)vp[2 * lane + 1];
+// ------------------------------------------------------------ dQ finalize
+// Per-step schedule, after the last ring step: dQ of a row is its running
+// fp32 sum of dS K over the main keys (the per-step launches), plus for a
+// branch row the branch-local terms, times the softmax scale.  One 16-lane
+// DPP row per query row (token x head, token order), a lane holding eight
+// dims; a branch row recomputes P and dS of its at most 64 branch keys from
+// the token-ordered Q and dO copies and the row statistics.
+__global__ __launch_bounds__(256) void bwd_dq_finalize_kernel(BwdParams p) {
+  const int lane = threadIdx.x & 63;
+  const int64_t rows = (int64_t)p.num_tokens * p.hq;
+  const int64_t R0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
+  const bool live = R0 < rows;
+  const int64_t R = live ? R0 : rows - 1;  // rows past the end redo the last row and write nothing
+  const int c8 = 8 * (lane & 15);
+  const int t = (int)(R / p.hq);
+  const int h = (int)(R - (int64_t)t * p.hq);
+  const TokInfo tk = p.toks[t];
+  const float* da = p.dq_acc + R * kHeadDim + c8;
+  const float4 a0 = *reinterpret_cast<const float4*>(da), a1 = *reinterpret_cast<const float4*>(da + 4);
+  float acc[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+
+  int nb = 0;
+  GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
+  if (tk.grp >= 0) {
+    gi = p.groups[tk.grp];
+    nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk.gidx + 1 : gi.len;
+  }
+  if (__ballot(nb > 0) != 0) {  // wavefront-uniform: some row of the wavefront is a branch row
+    const bf16x8 qv = ld16(p.qtok + R * kHeadDim + c8), gv = ld16(p.gtok + R * kHeadDim + c8);
+    const float2 rs = p.rowstat[R];  // (-LSE log2 e, -Delta)
+    float qf[8], gf[8];
 #pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        sdot += __shfl_xor(sdot, m);
-        pdot += __shfl_xor(pdot, m);
+    for (int e = 0; e < 8; ++e) {
+      qf[e] = (float)qv[e];
+      gf[e] = (float)gv[e];
+    }
+    const int64_t kvcol = (int64_t)(h / p.G) * kHeadDim + c8;
+    const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
+    for (int b = 0; __ballot(b < nb) != 0; ++b) {
+      const bool active = b < nb;
+      // inactive rows read their group's first key (main rows: branch row 0)
+      const int64_t krow = (int64_t)gi.row0 + (int64_t)(active ? b : 0) * gi.stride;
+      const bf16x8 kv = ld16(p.k_br + krow * kv_row_stride + kvcol);
+      const bf16x8 vv = ld16(p.v_br + krow * kv_row_stride + kvcol);
+      float sd = 0.f, pd = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        sd = fmaf(qf[e], (float)kv[e], sd);
+        pd = fmaf(gf[e], (float)vv[e], pd);
       }
-      const float pr = fast_exp2(sdot * p.scale_log2 + rs.x);  // rs.x = -LSE log2 e
-      const float ds = pr * (pdot + rs.y);  // rs.y = -Delta
-      atomicAdd(&acc_s[j * kHeadDim + 2 * lane], ds * q0);
-      atomicAdd(&acc_s[j * kHeadDim + 2 * lane + 1], ds * q1);
-      atomicAdd(&acc_s[(n + j) * kHeadDim + 2 * lane], pr * g0);
-      atomicAdd(&acc_s[(n + j) * kHeadDim + 2 * lane + 1], pr * g1);
+      sd = row16_sum(sd);
+      pd = row16_sum(pd);
+      const float pr = active ? fast_exp2(fmaf(sd, p.scale_log2, rs.x)) : 0.f;
+      const float ds = pr * (pd + rs.y);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = fmaf(ds, (float)kv[e], acc[e]);
     }
   }
-  __syncthreads();
-  for (int idx = tid; idx < n * kHeadDim; idx += blockDim.x) {
-    const int j = idx / kHeadDim, d = idx - j * kHeadDim;
-    const int64_t krow = (int64_t)gi.row0 + (int64_t)j * gi.stride;
-    const int64_t o = krow * kv_row_stride + kvh * kHeadDim + d;
-    store_grad(p.dk_br, o, acc_s[idx] * p.scale, p.grad_f32);
-    store_grad(p.dv_br, o, acc_s[n * kHeadDim + idx], p.grad_f32);
+  if (!live) return;
+  const int64_t orow = tk.qrow >= 0 ? tk.qrow : -tk.qrow - 1;
+  const int64_t o = (orow * p.hq + h) * kHeadDim + c8;
+  void* out = tk.qrow >= 0 ? p.dq_main : p.dq_br;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] *= p.scale;
+  if (p.grad_f32) {
+    float* d = static_cast<float*>(out) + o;
+    *reinterpret_cast<float4*>(d) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    *reinterpret_cast<float4*>(d + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  } else {
+    st16(static_cast<bf16*>(out) + o, pack8(acc[0], acc[1], acc[2], acc[3], acc[4], acc[5], acc[6], acc[7]));
+  }
+}
+
+// ------------------------------------------------------------ branch dK/dV
+// One wavefront per (group, KV head, block of four keys).  The wavefront's
+// four 16-lane rows each own one key j of the block, a lane holding eight
+// dims of K_j, V_j and of the dK_j, dV_j accumulators.  The member x head
+// rows (r = i G + h) of the group stream through all four lane rows at once
+// from the token-ordered Q and dO copies: every lane row computes its key's
+// score and dP with a 16-lane sum, forms P and dS (zero where the key is
+// hidden from the member: EAGLE-3 member i sees keys 0..i, a DFlash member
+// sees all) and accumulates dS q and P dO.  No atomics and no reduction
+// across lanes at the end: lane row j writes dK_j and dV_j once.  Rows are
+// loaded four at a time (four heads of one member) before any is used.
+namespace {
+
+constexpr int kBrKeys = 4;     // keys per wavefront
+constexpr int kBrWaves = 4;
+constexpr int kBrRows = 4;     // query rows loaded together
+
+struct BrRow {
+  bf16x8 q, g;
+  float2 rs;  // (-LSE log2 e, -Delta)
+};
+
+}  // namespace
+
+__global__ __launch_bounds__(64 * kBrWaves) void bwd_branch_kernel(BwdParams p, int key_blocks) {
+  const int lane = threadIdx.x & 63;
+  const int64_t unit = (int64_t)blockIdx.x * kBrWaves + (threadIdx.x >> 6);
+  const int64_t gk = unit / key_blocks;
+  const int kb = (int)(unit - gk * key_blocks);
+  if (gk >= (int64_t)p.num_groups * p.hkv) return;
+  const int g = (int)(gk / p.hkv);
+  const int kvh = (int)(gk - (int64_t)g * p.hkv);
+  const GroupInfo gi = p.groups[g];
+  const int n = gi.len;
+  if (kb * kBrKeys >= n) return;
+  const int G = p.G;
+  const bool eagle = gi.kind == BA_KIND_EAGLE_CHAIN;
+  const int j = kb * kBrKeys + (lane >> 4);  // this lane row's key
+  const int c8 = 8 * (lane & 15);            // this lane's first dim
+  const bool has_key = j < n;
+  const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
+  const int64_t krow = (int64_t)gi.row0 + (int64_t)(has_key ? j : 0) * gi.stride;
+  const int64_t kvoff = krow * kv_row_stride + kvh * kHeadDim + c8;
+  const bf16x8 kk = ld16(p.k_br + kvoff), vv = ld16(p.v_br + kvoff);
+  float kf[8], vf[8], dk[8], dv[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    kf[e] = (float)kk[e];
+    vf[e] = (float)vv[e];
+    dk[e] = 0.f;
+    dv[e] = 0.f;
+  }
+  // members that see at least one key of the block, four heads at a time
+  // (a member's G heads are consecutive rows of the token-ordered copies)
+  const int i_begin = eagle ? kb * kBrKeys : 0;
+  const int64_t head0 = (int64_t)kvh * G;
+  for (int i = i_begin; i < n; ++i) {
+    const bool vis = has_key && (!eagle || j <= i);
+    const int64_t trow0 = (int64_t)(gi.tok0 + i) * p.hq + head0;
+    for (int h0 = 0; h0 < G; h0 += kBrRows) {
+      BrRow rw[kBrRows];
+#pragma unroll
+      for (int u = 0; u < kBrRows; ++u) {
+        const int64_t trow = trow0 + (h0 + u < G ? h0 + u : h0);
+        rw[u] = BrRow{ld16(p.qtok + trow * kHeadDim + c8), ld16(p.gtok + trow * kHeadDim + c8), p.rowstat[trow]};
+      }
+      __builtin_amdgcn_sched_barrier(0);  // keep the loads together, ahead of their uses
+#pragma unroll
+      for (int u = 0; u < kBrRows; ++u) {
+        float qf[8], gf[8], sd = 0.f, pd = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          qf[e] = (float)rw[u].q[e];
+          gf[e] = (float)rw[u].g[e];
+          sd = fmaf(qf[e], kf[e], sd);
+          pd = fmaf(gf[e], vf[e], pd);
+        }
+        sd = row16_sum(sd);
+        pd = row16_sum(pd);
+        const float pr = vis && h0 + u < G ? fast_exp2(fmaf(sd, p.scale_log2, rw[u].rs.x)) : 0.f;  // -LSE log2 e
+        const float ds = pr * (pd + rw[u].rs.y);                                                   // -Delta
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          dk[e] = fmaf(ds, qf[e], dk[e]);
+          dv[e] = fmaf(pr, gf[e], dv[e]);
+        }
+      }
+    }
+  }
+  if (!has_key) return;
+  if (p.grad_f32) {
+    float* dkp = static_cast<float*>(p.dk_br) + kvoff;
+    float* dvp = static_cast<float*>(p.dv_br) + kvoff;
+    *reinterpret_cast<float4*>(dkp) = make_float4(dk[0] * p.scale, dk[1] * p.scale, dk[2] * p.scale, dk[3] * p.scale);
+    *reinterpret_cast<float4*>(dkp + 4) = make_float4(dk[4] * p.scale, dk[5] * p.scale, dk[6] * p.scale, dk[7] * p.scale);
+    *reinterpret_cast<float4*>(dvp) = make_float4(dv[0], dv[1], dv[2], dv[3]);
+    *reinterpret_cast<float4*>(dvp + 4) = make_float4(dv[4], dv[5], dv[6], dv[7]);
+  } else {
+    st16(static_cast<bf16*>(p.dk_br) + kvoff, pack8(dk[0] * p.scale, dk[1] * p.scale, dk[2] * p.scale, dk[3] * p.scale,
+                                                   dk[4] * p.scale, dk[5] * p.scale, dk[6] * p.scale, dk[7] * p.scale));
+    st16(static_cast<bf16*>(p.dv_br) + kvoff, pack8(dv[0], dv[1], dv[2], dv[3], dv[4], dv[5], dv[6], dv[7]));
   }
 }
 
@@ -1087,15 +1189,23 @@ hipError_t launch_bwd_dq(const BwdParams& p, int mode, hipStream_t stream) {
   if (p.num_qtiles == 0) return hipSuccess;
   dim3 grid(p.num_qtiles), block(256);
   if (mode == kModeStep) hipLaunchKernelGGL(bwd_dq_kernel<kModeStep>, grid, block, 0, stream, p);
-  else if (mode == kModeFinal) hipLaunchKernelGGL(bwd_dq_kernel<kModeFinal>, grid, block, 0, stream, p);
   else hipLaunchKernelGGL(bwd_dq_kernel<kModeFused>, grid, block, 0, stream, p);
   return hipGetLastError();
 }
 
+hipError_t launch_bwd_dq_finalize(const BwdParams& p, hipStream_t stream) {
+  const int64_t threads = (int64_t)p.num_tokens * p.hq * 16;
+  if (threads == 0) return hipSuccess;
+  hipLaunchKernelGGL(bwd_dq_finalize_kernel, dim3(grid_for(threads)), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_bwd_branch(const BwdParams& p, int max_group_len, hipStream_t stream) {
-  if (p.num_groups == 0) return hipSuccess;
-  const size_t lds = (size_t)2 * max_group_len * kHeadDim * sizeof(float);
-  hipLaunchKernelGGL(bwd_branch_kernel, dim3(p.num_groups * p.hkv), dim3(256), lds, stream, p);
+  if (p.num_groups == 0 || max_group_len <= 0) return hipSuccess;
+  const int key_blocks = (max_group_len + kBrKeys - 1) / kBrKeys;
+  const int64_t units = (int64_t)p.num_groups * p.hkv * key_blocks;
+  const int64_t blocks = (units + kBrWaves - 1) / kBrWaves;
+  hipLaunchKernelGGL(bwd_branch_kernel, dim3((unsigned)blocks), dim3(64 * kBrWaves), 0, stream, p, key_blocks);
   return hipGetLastError();
 }
 

@@ -270,6 +270,20 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+template <int Ctrl>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), Ctrl, 0xF, 0xF, true));
+}
+// Sum over the 16 lanes of a DPP row (lanes 16r .. 16r+15); every lane of
+// the row receives the sum.  All lanes of the wavefront must be active.
+__device__ __forceinline__ float row16_sum(float x) {
+  x += dpp_mov<0x128>(x);  // row_ror:8
+  x += dpp_mov<0x124>(x);  // row_ror:4
+  x += dpp_mov<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp_mov<0xB1>(x);   // quad_perm [1,0,3,2]
+  return x;
+}
+
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 

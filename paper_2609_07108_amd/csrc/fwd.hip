@@ -28,13 +28,14 @@
 //
 // Epilogues
 //   STEP  : merge the step's partial (O, LSE) into the running fp32 pair in
-//           the workspace with Eq. lse-merge (first step writes it).
-//   FINAL : read the running pair back as the main-sequence partial.
+//           the workspace with Eq. lse-merge (first step writes it); after
+//           the last step fwd_finalize_kernel takes the running pair as the
+//           main-sequence partial.
 //   FUSED : all ring steps in one pass; the running pair stays in registers.
-// FINAL and FUSED then compute the branch-local partial of every branch row
-// (chain members 0..i, or the whole block; at most 64 keys, on the vector
-// ALUs), merge it with the main partial by Eq. lse-merge and write bf16 O and
-// the natural-log LSE.
+// FUSED and the finalize kernel compute the branch-local partial of every
+// branch row (chain members 0..i, or the whole block; at most 64 keys, on
+// the vector ALUs), merge it with the main partial by Eq. lse-merge and
+// write bf16 O and the natural-log LSE.
 #include <type_traits>
 
 #include "ba_internal.h"
@@ -92,21 +93,15 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
   f32x16 o[2][4];  // O^T accumulators, d = 32 dt + 8 (v/4) + 4 half + v%4
   float m_use[2] = {-INFINITY, -INFINITY};  // reference maximum of the exponentials (log2)
   float lsum[2] = {0.f, 0.f};               // this lane's share of the row sum
-  if constexpr (MODE == kModeFinal) {
-    // no ring walk: no MFMA ever accumulates into O here
-    for (int rb = 0; rb < 2; ++rb)
-      for (int dt = 0; dt < 4; ++dt) o[rb][dt] = f32x16{};
-  } else {
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(o[rb][dt]);
-  }
+    for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(o[rb][dt]);
 
   const int Pmin = p.toks[tile.tok_begin].P;
   const int Pmax = p.toks[tile.tok_begin + tile.ntok - 1].P;
 
-  if (MODE != kModeFinal) {
+  {
     // ---- cursor over (ring step, 64-key tile): ring step i brings block
     // j = (rank - i) mod C; tiles cover the prefix of the block that the
     // tile's largest causal limit can see
@@ -403,32 +398,13 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
 
     // main-sequence partial: normalised output in st_o, LSE (log2) in lse_m
     float lse_m;
-    if (MODE == kModeFinal) {
-      if (valid[rb]) {
-        const float* oacc = p.o_acc + acc_row * kHeadDim;
+    if (l_tot[rb] > 0.f) {
+      lse_m = m_use[rb] + __log2f(l_tot[rb]);
+      const float inv = 1.f / l_tot[rb];
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-          for (int vq = 0; vq < 4; ++vq) {
-            const float4 a = *reinterpret_cast<const float4*>(oacc + 32 * dt + 8 * vq + 4 * half);
-            st_o[dt][4 * vq + 0] = a.x;
-            st_o[dt][4 * vq + 1] = a.y;
-            st_o[dt][4 * vq + 2] = a.z;
-            st_o[dt][4 * vq + 3] = a.w;
-          }
-        lse_m = p.lse_acc[acc_row];
-      } else {
-        lse_m = -INFINITY;
-      }
+      for (int dt = 0; dt < 4; ++dt) st_o[dt] *= inv;
     } else {
-      if (l_tot[rb] > 0.f) {
-        lse_m = m_use[rb] + __log2f(l_tot[rb]);
-        const float inv = 1.f / l_tot[rb];
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) st_o[dt] *= inv;
-      } else {
-        lse_m = -INFINITY;
-      }
+      lse_m = -INFINITY;
     }
 
     // ---- branch-local partial (vector ALUs; at most 64 keys per row)
@@ -512,11 +488,106 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
   finish(1);
 }
 
+// ------------------------------------------------------------ finalize
+// Per-step schedule, after the last ring step: the running pair (O, LSE) of
+// every query row is its main-sequence partial.  One 16-lane DPP row per
+// query row (token x head, token order), a lane holding eight dims.  Branch
+// rows add their branch-local partial (online softmax over chain members
+// 0..i or the whole block, at most 64 keys) and merge it with the main
+// partial by Eq. lse-merge; every row is written as bf16 O and natural-log
+// LSE.  Memory-bound: the running fp32 O is read once, O written once.
+__global__ __launch_bounds__(256) void fwd_finalize_kernel(FwdParams p) {
+  const int lane = threadIdx.x & 63;
+  const int64_t rows = (int64_t)p.num_tokens * p.hq;
+  const int64_t R0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
+  const bool live = R0 < rows;
+  const int64_t R = live ? R0 : rows - 1;  // rows past the end redo the last row and write nothing
+  const int c8 = 8 * (lane & 15);
+  const int t = (int)(R / p.hq);
+  const int h = (int)(R - (int64_t)t * p.hq);
+  const TokInfo tk = p.toks[t];
+  const float* oa = p.o_acc + R * kHeadDim + c8;
+  const float4 a0 = *reinterpret_cast<const float4*>(oa), a1 = *reinterpret_cast<const float4*>(oa + 4);
+  const float om[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+  const float lse_m = p.lse_acc[R];  // log2 units; -inf: no main key
+
+  int nb = 0;
+  GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
+  if (tk.grp >= 0) {
+    gi = p.groups[tk.grp];
+    nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk.gidx + 1 : gi.len;
+  }
+  float mb = -INFINITY, lb = 0.f, ob[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ob[e] = 0.f;
+  if (__ballot(nb > 0) != 0) {  // wavefront-uniform: some row of the wavefront is a branch row
+    const int64_t qr = tk.qrow >= 0 ? tk.qrow : -tk.qrow - 1;
+    const bf16x8 qv = ld16((tk.qrow >= 0 ? p.q_main : p.q_br) + (qr * p.hq + h) * kHeadDim + c8);
+    float qf[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qf[e] = (float)qv[e];
+    const int64_t kvcol = (int64_t)(h / p.G) * kHeadDim + c8;
+    const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
+    for (int b = 0; __ballot(b < nb) != 0; ++b) {
+      const bool active = b < nb;
+      // inactive rows read their group's first key (main rows: branch row 0)
+      const int64_t krow = (int64_t)gi.row0 + (int64_t)(active ? b : 0) * gi.stride;
+      const bf16x8 kv = ld16(p.k_br + krow * kv_row_stride + kvcol);
+      const bf16x8 vv = ld16(p.v_br + krow * kv_row_stride + kvcol);
+      float dot = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dot = fmaf(qf[e], (float)kv[e], dot);
+      dot = row16_sum(dot);
+      if (active) {
+        const float x = dot * p.scale_log2;
+        const float m_new = fmaxf(mb, x);
+        const float alpha = fast_exp2(mb - m_new);
+        const float ex = fast_exp2(x - m_new);
+        lb = lb * alpha + ex;
+        mb = m_new;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ob[e] = fmaf(ob[e], alpha, ex * (float)vv[e]);
+      }
+    }
+  }
+  if (!live) return;
+
+  // Eq. lse-merge of the main and branch partials (log2 units)
+  const float lse_b = lb > 0.f ? mb + __log2f(lb) : -INFINITY;
+  const float hi = fmaxf(lse_m, lse_b);
+  const float wm = lse_m == -INFINITY ? 0.f : fast_exp2(lse_m - hi);
+  const float wbr = lse_b == -INFINITY ? 0.f : fast_exp2(lse_b - hi);
+  const float tot = wm + wbr;
+  const float lse2 = tot > 0.f ? hi + __log2f(tot) : -INFINITY;
+  const float cm = tot > 0.f ? wm / tot : 0.f;
+  const float cb = lb > 0.f ? wbr / (tot * lb) : 0.f;
+  bf16* out;
+  float* lse_out;
+  if (tk.qrow >= 0) {
+    out = p.o_main + ((int64_t)tk.qrow * p.hq + h) * kHeadDim;
+    lse_out = p.lse_main + (int64_t)h * p.n_local + tk.qrow;
+  } else {
+    const int64_t br = -tk.qrow - 1;
+    out = p.o_br + (br * p.hq + h) * kHeadDim;
+    lse_out = p.lse_br + (int64_t)h * p.n_br + br;
+  }
+  st16(out + c8, pack8(cm * om[0] + cb * ob[0], cm * om[1] + cb * ob[1], cm * om[2] + cb * ob[2],
+                       cm * om[3] + cb * ob[3], cm * om[4] + cb * ob[4], cm * om[5] + cb * ob[5],
+                       cm * om[6] + cb * ob[6], cm * om[7] + cb * ob[7]));
+  if ((lane & 15) == 0) *lse_out = lse2 * kLn2;
+}
+
+hipError_t launch_fwd_finalize(const FwdParams& p, hipStream_t stream) {
+  const int64_t threads = (int64_t)p.num_tokens * p.hq * 16;
+  if (threads == 0) return hipSuccess;
+  hipLaunchKernelGGL(fwd_finalize_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_fwd(const FwdParams& p, int mode, hipStream_t stream) {
   if (p.num_tiles == 0) return hipSuccess;
   dim3 grid(p.num_tiles), block(256);
   if (mode == kModeStep) hipLaunchKernelGGL(fwd_kernel<kModeStep>, grid, block, 0, stream, p);
-  else if (mode == kModeFinal) hipLaunchKernelGGL(fwd_kernel<kModeFinal>, grid, block, 0, stream, p);
   else hipLaunchKernelGGL(fwd_kernel<kModeFused>, grid, block, 0, stream, p);
   return hipGetLastError();
 }

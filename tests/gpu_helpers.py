@@ -113,3 +113,9 @@ def assert_bwd_close(gpu, ref, tol=GRAD_TOL):
         assert np.all(np.isfinite(a)), f"{name}: non-finite values"
         e = rel_l2(a, r)
         assert e <= tol, f"{name}: relative L2 error {e:.3e} > {tol}"
+        # stricter than the bar: the main and the branch part each on its own,
+        # so a wrong branch-local gradient cannot hide under the main one
+        for part in (m, b):
+            if gpu[part].size and np.linalg.norm(ref[part]) > 0:
+                e = rel_l2(gpu[part].ravel(), ref[part].ravel())
+                assert e <= tol, f"{name} ({part}): relative L2 error {e:.3e} > {tol}"
