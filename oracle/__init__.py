@@ -18,9 +18,13 @@ reduction to textbook causal attention (torch SDPA in float64), the Q = 0
 closed form of every row's key count, the merge identity of Eq. lse-merge,
 the chain rule through the merge, central finite differences, reassembly of
 all context-parallel ranks, and the closed-form zigzag pair counts.
+:mod:`oracle.rope` adds rotary position embedding in front of the op
+(pinned against the Llama rotary routine of the transformers library, the
+relative-position identity and finite differences).
 """
 
 from .attention import (  # noqa: F401
     KIND_EAGLE, KIND_DFLASH, owner_rank, select_queries, forward, backward,
     lse_merge, lse_merge_backward, allowed_pair_counts, useful_flops,
 )
+from . import rope  # noqa: F401

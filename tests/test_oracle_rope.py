@@ -1,0 +1,147 @@
+"""Pins of the RoPE oracle (rotary position embedding in front of branch
+attention, `oracle.rope`).
+
+R1 the Llama rotary routine of the transformers library (its cos/sin tables
+and `apply_rotary_pos_emb`, a library special case), R2 the relative-position
+identity that defines rotary embeddings, R3 orthogonality and the inverse,
+R4 shift invariance of the whole attention output, R5 central finite
+differences through rotation + attention (pins the transposed rotation of
+the gradients).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import rope
+from paper_2609_07108_amd import workloads as W
+
+TENSORS = ("qm", "km", "vm", "qb", "kb", "vb")
+
+
+def draw_all(p):
+    return {k: p.draw(k).float().numpy().astype(np.float64) for k in TENSORS}
+
+
+@pytest.mark.parametrize("head_dim,theta", [(128, 1.0e4), (128, 5.0e5), (8, 1.0e4)])
+def test_r1_matches_llama_rotary_routine(head_dim, theta):
+    from transformers import LlamaConfig
+    from transformers.models.llama.modeling_llama import LlamaRotaryEmbedding, apply_rotary_pos_emb
+
+    rng = np.random.default_rng(71)
+    pos = np.r_[0, 1, 2, 7, 64, 127, 128, rng.integers(0, 300, 9)]
+    x = rng.standard_normal((len(pos), 3, head_dim))
+    cfg = LlamaConfig(hidden_size=2 * head_dim, num_attention_heads=2, num_key_value_heads=2,
+                      head_dim=head_dim, rope_theta=theta)
+    emb = LlamaRotaryEmbedding(config=cfg)
+    cos, sin = emb(torch.zeros(1, dtype=torch.float32), torch.as_tensor(pos)[None])
+    xt = torch.as_tensor(x).permute(1, 0, 2)[None]  # [1, H, rows, d]
+    ref, _ = apply_rotary_pos_emb(xt, xt, cos.double(), sin.double())
+    ref = ref[0].permute(1, 0, 2).numpy()
+    got = rope.rotate(x, pos, theta)
+    # the library tabulates cos / sin in float32 from float32 angles
+    assert np.max(np.abs(got - ref)) <= 5e-5 * np.max(np.abs(x))
+    # and the rotation is not the identity or a reflection
+    assert np.max(np.abs(got - x)) > 0.1
+    assert np.max(np.abs(rope.rotate(x, pos, theta, inverse=True) - ref)) > 0.1
+
+
+def test_r2_relative_position_identity():
+    rng = np.random.default_rng(72)
+    n = 32
+    q = rng.standard_normal((n, 1, 128))
+    k = rng.standard_normal((n, 1, 128))
+    m = rng.integers(0, 300000, n)
+    p = rng.integers(0, 300000, n)
+    t = rng.integers(-20000, 20000, n)
+    for theta in (1.0e4, 1.0e6):
+        a = np.sum(rope.rotate(q, m, theta) * rope.rotate(k, p, theta), axis=-1)
+        b = np.sum(rope.rotate(q, m + t, theta) * rope.rotate(k, p + t, theta), axis=-1)
+        c = np.sum(rope.rotate(q, m - p, theta) * k, axis=-1)
+        assert np.max(np.abs(a - b)) <= 1e-8 * np.max(np.abs(a))
+        assert np.max(np.abs(a - c)) <= 1e-8 * np.max(np.abs(a))
+
+
+def test_r3_orthogonal_with_transposed_inverse():
+    rng = np.random.default_rng(73)
+    x = rng.standard_normal((40, 4, 128))
+    pos = rng.integers(0, 262144, 40)
+    y = rope.rotate(x, pos, 5.0e5)
+    assert np.allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-12)
+    assert np.allclose(rope.rotate(y, pos, 5.0e5, inverse=True), x, atol=1e-12)
+    # <R x, y> == <x, R^T y>
+    z = rng.standard_normal(x.shape)
+    lhs = np.sum(rope.rotate(x, pos, 5.0e5) * z)
+    rhs = np.sum(x * rope.rotate(z, pos, 5.0e5, inverse=True))
+    assert abs(lhs - rhs) <= 1e-10 * abs(lhs)
+
+
+def test_r4_attention_depends_on_relative_positions_only():
+    p = W.custom([64, 32], [("eagle", 3), ("dflash", 4, 16)], hq=4, hkv=2, head_dim=16,
+                 cp_size=2, cp_rank=1, seed=74)
+    t = draw_all(p)
+    pm, pb = rope.positions(p, len(t["qb"]))
+    theta = 1.0e4
+    res = []
+    for shift in (0, 100000):
+        # one shift per sequence keeps every relative position within a sequence
+        cu = np.asarray(p.cu_seqlens)
+        sm = pm + shift * np.searchsorted(cu, np.arange(len(pm)), side="right")
+        sb = pb + shift * (1 + np.asarray(p.g_seq)[np.searchsorted(np.asarray(p.g_row0), np.arange(len(pb)),
+                                                                    side="right") - 1])
+        res.append(oracle.forward(p, rope.rotate(t["qm"], sm, theta), rope.rotate(t["km"], sm, theta), t["vm"],
+                                  rope.rotate(t["qb"], sb, theta), rope.rotate(t["kb"], sb, theta), t["vb"]))
+    for a, b in zip(res[0], res[1]):
+        fin = np.isfinite(a)
+        assert np.array_equal(fin, np.isfinite(b))
+        assert np.max(np.abs(a[fin] - b[fin])) <= 1e-9
+    # and rotation does change the result
+    plain = oracle.forward(p, *[t[k] for k in TENSORS])
+    assert np.max(np.abs(plain[0] - res[0][0])) > 1e-3
+
+
+def test_positions_follow_the_anchor():
+    p = W.custom([32], [("eagle", 3)], hq=1, hkv=1, head_dim=4, cp_size=1, seed=75)
+    pm, pb = rope.positions(p)
+    assert np.array_equal(pm, np.arange(32))
+    for g in range(len(p.g_len)):
+        r0, a = int(p.g_row0[g]), int(p.g_anchor[g])
+        assert list(pb[r0:r0 + int(p.g_len[g])]) == [a + 1, a + 2, a + 3]
+
+
+def _loss(p, t, dom, dob, mq, bq, theta):
+    om, _, ob, _ = rope.forward(p, *[t[k] for k in TENSORS], theta, main_q=mq, br_q=bq)
+    return float(np.sum(om * dom) + np.sum(ob * dob))
+
+
+def test_r5_finite_differences_through_rotation():
+    p = W.custom([32, 16], [("eagle", 2), ("dflash", 4, 8)], hq=2, hkv=1, head_dim=8,
+                 cp_size=2, cp_rank=0, seed=76)
+    theta = 50.0  # large angles even at these short lengths
+    t = draw_all(p)
+    mq, bq = oracle.select_queries(p)
+    rng = np.random.default_rng(77)
+    dom = rng.standard_normal((len(mq), p.hq, p.head_dim))
+    dob = rng.standard_normal((len(bq), p.hq, p.head_dim))
+    g = rope.backward(p, *[t[k] for k in TENSORS], dom, dob, theta, main_q=mq, br_q=bq)
+    h = 1e-6
+    for name, grad_name, rows in (("qm", "dq_main", mq), ("qb", "dq_br", bq), ("km", "dk_main", None),
+                                  ("vm", "dv_main", None), ("kb", "dk_br", None), ("vb", "dv_br", None)):
+        for _ in range(6):
+            if rows is not None:
+                gi = int(rng.integers(len(rows)))
+                row = int(rows[gi])
+            else:
+                row = gi = int(rng.integers(len(t[name])))
+            hh = int(rng.integers(t[name].shape[1]))
+            dd = int(rng.integers(p.head_dim))
+            old = t[name][row, hh, dd]
+            t[name][row, hh, dd] = old + h
+            lp = _loss(p, t, dom, dob, mq, bq, theta)
+            t[name][row, hh, dd] = old - h
+            lm = _loss(p, t, dom, dob, mq, bq, theta)
+            t[name][row, hh, dd] = old
+            fd = (lp - lm) / (2 * h)
+            an = g[grad_name][gi, hh, dd]
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, row, hh, dd, fd, an)
