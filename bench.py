@@ -141,6 +141,9 @@ def main():
     ap.add_argument("--mode", choices=["fused", "per_step"], default="per_step",
                     help="per_step: one launch per ring step (the ring's schedule); fused: one walk over all blocks")
     ap.add_argument("--cpu-rows", type=int, default=24, help="oracle sample size (0 disables)")
+    ap.add_argument("--rope", type=float, default=0.0, metavar="THETA",
+                    help="rotate queries and keys by their positions (rotary embedding, base THETA) "
+                         "in front of the attention; 0 (default) leaves them as they are")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB mebibytes (HBM counter calibration)")
     args = ap.parse_args()
@@ -169,7 +172,7 @@ def main():
     prob = W.config(args.config)
     mode = B.BA_MODE_FUSED if args.mode == "fused" else B.BA_MODE_PER_STEP
     t0 = time.perf_counter()
-    share = RS.build_share(prob, device="cuda:0", with_grad=True)
+    share = RS.build_share(prob, device="cuda:0", with_grad=True, rope_theta=args.rope)
     out = RS.alloc_outputs(share, grads=True)
     ws = RS.workspace(share, mode, backward=True)
     torch.cuda.synchronize()
@@ -232,14 +235,15 @@ def main():
         cpu = cpu_baseline(prob, args.cpu_rows)
 
     n_local, ntok = share.plan.info()
-    traffic = measured_traffic(dom_name, prob.name, args.mode)
+    traffic = measured_traffic(dom_name, prob.name, args.mode) if not args.rope else None
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": prob.name, "describe": prob.describe, "mode": args.mode,
                    "query_rows": ntok, "main_keys": prob.n_main, "hq": prob.hq, "hkv": prob.hkv,
-                   "head_dim": d, "cp_size": prob.cp_size, "cp_rank": prob.cp_rank},
+                   "head_dim": d, "cp_size": prob.cp_size, "cp_rank": prob.cp_rank,
+                   "rope_theta": args.rope},
         "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "useful_tflop_per_step": {"fwd": round(f_fwd / 1e12, 3), "bwd": round(f_bwd / 1e12, 3)},
         "ring_ms": {"fwd": round(fwd_ring_ms, 3), "bwd": round(bwd_ring_ms, 3)},

@@ -196,6 +196,25 @@ int zigzag_partition(const int32_t* cu_seqlens, int32_t num_seqs, int32_t cp_siz
 int branch_attn_plan_create(const ba_problem* prob, ba_plan** out);
 void branch_attn_plan_destroy(ba_plan* plan);
 
+/* Rotary position embedding in front of the attention: the step before the
+ * op inside a draft layer, whose queries and keys are rotated by their
+ * positions.  The paper gives no positional scheme for branch tokens; this
+ * library's reading: a main token at position p of its sequence has
+ * position p, member i (0-based) of a branch group anchored at a has
+ * position a + 1 + i (an EAGLE-3 member of depth i + 1, or block position
+ * i + 1 of a DFlash block, after its anchor).  Dims j and j + 64 (j < 64)
+ * turn together by the angle pos * theta^(-j/64) (x_j' = x_j cos - x_{j+64}
+ * sin, x_{j+64}' = x_{j+64} cos + x_j sin); the rotated queries and keys are
+ * rounded to bf16 (RNE) before attending, values are not rotated.
+ * With theta > 0 every later branch_attn_fwd / branch_attn_bwd call on the
+ * plan attends the rotated queries and keys, and the backward returns dQ and
+ * dK with respect to the unrotated inputs (the transposed rotation of the
+ * gradients of the rotated ones).  theta = 0 turns the rotation off.  The
+ * plan's workspace sizes grow (query them again): rotated copies of Q and K,
+ * and fp32 staging of the gradients.  Host only.  BA_E_INVAL for a negative
+ * or non-finite theta, BA_E_UNSUPPORTED if a position reaches 2^24. */
+int branch_attn_plan_set_rope(ba_plan* plan, float theta);
+
 /* Workspace bytes needed by branch_attn_fwd / branch_attn_bwd in `mode`. */
 int branch_attn_workspace_size(const ba_plan* plan, int32_t mode, size_t* fwd_bytes,
                                size_t* bwd_bytes);

@@ -63,27 +63,43 @@ def rotate(x, pos, theta: float, inverse: bool = False):
     return np.concatenate([lo * c - hi * s, hi * c + lo * s], axis=-1)
 
 
-def forward(prob, qm, km, vm, qb, kb, vb, theta: float, **kw):
-    """Branch attention of the rotated queries and keys (see
-    :func:`attention.forward` for the arguments and results)."""
+def round_bf16(x):
+    """Round to the nearest bfloat16 value (8 significant bits, ties to
+    even); values are assumed inside bfloat16's normal range or zero."""
+    x = np.asarray(x, np.float64)
+    m, e = np.frexp(x)  # x = m 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(m * 256.0) / 256.0, e)
+
+
+def _rotated_inputs(prob, qm, km, qb, kb, theta, rounded):
     pm, pb = positions(prob, len(np.asarray(qb)))
-    return attention.forward(prob, rotate(qm, pm, theta), rotate(km, pm, theta), vm,
-                             rotate(qb, pb, theta), rotate(kb, pb, theta), vb, **kw)
+    rq = round_bf16 if rounded else (lambda a: a)
+    return (rq(rotate(qm, pm, theta)), rq(rotate(km, pm, theta)), rq(rotate(qb, pb, theta)),
+            rq(rotate(kb, pb, theta)), pm, pb)
 
 
-def backward(prob, qm, km, vm, qb, kb, vb, dom, dob, theta: float, main_q=None, br_q=None, **kw):
+def forward(prob, qm, km, vm, qb, kb, vb, theta: float, rounded: bool = False, **kw):
+    """Branch attention of the rotated queries and keys (see
+    :func:`attention.forward` for the arguments and results).  ``rounded``
+    rounds the rotated queries and keys to bfloat16 before attending (a
+    draft layer computing in bfloat16 hands them over in that type)."""
+    rqm, rkm, rqb, rkb, _, _ = _rotated_inputs(prob, qm, km, qb, kb, theta, rounded)
+    return attention.forward(prob, rqm, rkm, vm, rqb, rkb, vb, **kw)
+
+
+def backward(prob, qm, km, vm, qb, kb, vb, dom, dob, theta: float, main_q=None, br_q=None,
+             rounded: bool = False, **kw):
     """Gradients with respect to the unrotated inputs: the attention backward
-    on the rotated inputs, then the transposed rotation of dQ and dK."""
+    on the rotated inputs, then the transposed rotation of dQ and dK (the
+    bfloat16 rounding of ``rounded`` passes gradients through unchanged)."""
     if main_q is None or br_q is None:
         mq0, bq0 = attention.select_queries(prob)
         main_q = mq0 if main_q is None else main_q
         br_q = bq0 if br_q is None else br_q
     main_q = np.asarray(main_q, np.int64)
     br_q = np.asarray(br_q, np.int64)
-    pm, pb = positions(prob, len(np.asarray(qb)))
-    g = attention.backward(prob, rotate(qm, pm, theta), rotate(km, pm, theta), vm,
-                           rotate(qb, pb, theta), rotate(kb, pb, theta), vb, dom, dob,
-                           main_q=main_q, br_q=br_q, **kw)
+    rqm, rkm, rqb, rkb, pm, pb = _rotated_inputs(prob, qm, km, qb, kb, theta, rounded)
+    g = attention.backward(prob, rqm, rkm, vm, rqb, rkb, vb, dom, dob, main_q=main_q, br_q=br_q, **kw)
     g["dq_main"] = rotate(g["dq_main"], pm[main_q], theta, inverse=True)
     g["dq_br"] = rotate(g["dq_br"], pb[br_q], theta, inverse=True)
     g["dk_main"] = rotate(g["dk_main"], pm, theta, inverse=True)

@@ -33,7 +33,7 @@ BA_MODE_FUSED = 1
 EXPORTED = ("zigzag_partition", "branch_attn_plan_create", "branch_attn_plan_destroy",
             "branch_attn_workspace_size", "branch_attn_plan_info", "branch_attn_useful_flops",
             "branch_attn_pair_counts", "branch_attn_last_error", "branch_attn_fwd", "branch_attn_bwd",
-            "lse_merge")
+            "lse_merge", "branch_attn_plan_set_rope")
 
 c_i32 = ctypes.c_int32
 c_vp = ctypes.c_void_p
@@ -89,6 +89,7 @@ def lib() -> ctypes.CDLL:
         L.branch_attn_plan_create.argtypes = [ctypes.POINTER(BaProblem), ctypes.POINTER(c_vp)]
         L.branch_attn_plan_destroy.argtypes = [c_vp]
         L.branch_attn_plan_destroy.restype = None
+        L.branch_attn_plan_set_rope.argtypes = [c_vp, ctypes.c_float]
         L.branch_attn_workspace_size.argtypes = [c_vp, c_i32, ctypes.POINTER(ctypes.c_size_t),
                                                  ctypes.POINTER(ctypes.c_size_t)]
         L.branch_attn_plan_info.argtypes = [c_vp, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
@@ -168,6 +169,10 @@ class Plan:
         if h is not None and h.value and _lib is not None:
             _lib.branch_attn_plan_destroy(h)
             self._h = None
+
+    def set_rope(self, theta: float):
+        """Rotary position embedding in front of the attention (theta 0: off)."""
+        _check(lib().branch_attn_plan_set_rope(self._h, float(theta)))
 
     def workspace_size(self, mode: int):
         f, b = ctypes.c_size_t(), ctypes.c_size_t()

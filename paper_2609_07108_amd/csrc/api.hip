@@ -72,6 +72,56 @@ Common prepare(const ba_plan* plan, int32_t mode, void* workspace, size_t ws_byt
   return c;
 }
 
+// Rotary embedding tables of a plan inside the workspace copy of its image.
+struct RopeTables {
+  const int32_t* pos_block;  // [C][n_local]
+  const int32_t* pos_qmain;  // [n_local]
+  const int32_t* pos_br;     // [num_branch_rows]
+  const RopeFreq* freq;
+};
+
+RopeTables rope_tables(const Plan& P, const Common& c) {
+  const char* t = c.ws + c.w.tables;
+  return RopeTables{reinterpret_cast<const int32_t*>(t + P.off_pos_block),
+                    reinterpret_cast<const int32_t*>(t + P.off_pos_qmain),
+                    reinterpret_cast<const int32_t*>(t + P.off_pos_br),
+                    reinterpret_cast<const RopeFreq*>(t + P.off_freq)};
+}
+
+// Rotated bf16 copies of the queries and keys of one call; the pointers the
+// kernels read are redirected to them.
+template <typename Params>
+hipError_t rotate_inputs(const Plan& P, const Common& c, const void* q_main, const void* q_br, const void* k_br,
+                         const void* const* k_step, bool has_main, bool has_br, bool has_keys, Params& p,
+                         hipStream_t stream) {
+  const RopeTables rt = rope_tables(P, c);
+  const int64_t nl = P.n_local, nb = P.num_branch_rows;
+  const int64_t krow = (int64_t)P.hkv * kHeadDim;
+  hipError_t e = hipSuccess;
+  if (has_main) {
+    bf16* rq = reinterpret_cast<bf16*>(c.ws + c.w.rq_main);
+    if ((e = launch_rope_rows(static_cast<const bf16*>(q_main), rq, rt.pos_qmain, rt.freq, nl, P.hq, stream)))
+      return e;
+    p.q_main = rq;
+  }
+  if (has_br) {
+    bf16* rq = reinterpret_cast<bf16*>(c.ws + c.w.rq_br);
+    bf16* rk = reinterpret_cast<bf16*>(c.ws + c.w.rk_br);
+    if ((e = launch_rope_rows(static_cast<const bf16*>(q_br), rq, rt.pos_br, rt.freq, nb, P.hq, stream))) return e;
+    if ((e = launch_rope_rows(static_cast<const bf16*>(k_br), rk, rt.pos_br, rt.freq, nb, P.hkv, stream))) return e;
+    p.q_br = rq;
+    p.k_br = rk;
+  }
+  for (int j = 0; j < P.cp_size && has_keys; ++j) {
+    bf16* rk = reinterpret_cast<bf16*>(c.ws + c.w.rk_step) + (int64_t)j * nl * krow;
+    if ((e = launch_rope_rows(static_cast<const bf16*>(k_step[j]), rk, rt.pos_block + (int64_t)j * nl, rt.freq, nl,
+                              P.hkv, stream)))
+      return e;
+    p.k_step[j] = rk;
+  }
+  return e;
+}
+
 }  // namespace
 }  // namespace ba
 
@@ -127,6 +177,9 @@ extern "C" int branch_attn_fwd(void* stream_, const ba_plan* plan, int32_t mode,
   p.lse_main = io->lse_main;
   p.lse_br = io->lse_br;
   hipError_t e;
+  if (P.rope_theta > 0.f &&
+      (e = rotate_inputs(P, c, io->q_main, io->q_br, io->k_br, io->k_step, has_main, has_br, has_keys, p, stream)))
+    return hip_fail(e, "rotary embedding launch");
   if ((e = record(io->ring_begin, stream)) != hipSuccess) return hip_fail(e, "event record");
   if (mode == BA_MODE_FUSED) {
     p.step_first = 0;
@@ -189,9 +242,22 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
   if (P.toks.empty() && !has_keys) return BA_OK;
   c = prepare(plan, mode, workspace, workspace_bytes, true, stream);
   if (c.rc) return c.rc;
+  const bool rope = P.rope_theta > 0.f;
+  const int64_t krow = (int64_t)P.hkv * kHeadDim;
+  float* gk_step = rope ? reinterpret_cast<float*>(c.ws + c.w.gk_step) : nullptr;
+  float* gv_step = rope ? reinterpret_cast<float*>(c.ws + c.w.gv_step) : nullptr;
   for (int j = 0; j < P.cp_size && has_keys; ++j) {
-    if ((e = launch_zero(io->dk_step[j], step_bytes, stream)) != hipSuccess) return hip_fail(e, "clear dk");
-    if ((e = launch_zero(io->dv_step[j], step_bytes, stream)) != hipSuccess) return hip_fail(e, "clear dv");
+    if (rope && !P.toks.empty()) {
+      // gradients of the rotated keys are staged in fp32 and rotated back at the end
+      p.dk_step[j] = gk_step + (int64_t)j * P.n_local * krow;
+      p.dv_step[j] = gv_step + (int64_t)j * P.n_local * krow;
+      const size_t f32_bytes = (size_t)P.n_local * krow * sizeof(float);
+      if ((e = launch_zero(p.dk_step[j], f32_bytes, stream)) != hipSuccess) return hip_fail(e, "clear dk");
+      if ((e = launch_zero(p.dv_step[j], f32_bytes, stream)) != hipSuccess) return hip_fail(e, "clear dv");
+    } else {
+      if ((e = launch_zero(io->dk_step[j], step_bytes, stream)) != hipSuccess) return hip_fail(e, "clear dk");
+      if ((e = launch_zero(io->dv_step[j], step_bytes, stream)) != hipSuccess) return hip_fail(e, "clear dv");
+    }
   }
   if (P.toks.empty()) return BA_OK;
   p.seqs = reinterpret_cast<const SeqInfo*>(c.ws + c.w.tables + P.off_seqs);
@@ -230,6 +296,15 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
   p.qtok = reinterpret_cast<bf16*>(c.ws + c.w.qtok);
   p.gtok = reinterpret_cast<bf16*>(c.ws + c.w.gtok);
   p.dq_acc = mode == BA_MODE_PER_STEP ? reinterpret_cast<float*>(c.ws + c.w.dq_acc) : nullptr;
+  if (rope) {
+    if ((e = rotate_inputs(P, c, io->q_main, io->q_br, io->k_br, io->k_step, has_main, has_br, has_keys, p, stream)))
+      return hip_fail(e, "rotary embedding launch");
+    p.dq_main = c.ws + c.w.gq_main;
+    p.dq_br = c.ws + c.w.gq_br;
+    p.dk_br = c.ws + c.w.gk_br;
+    p.dv_br = c.ws + c.w.gv_br;
+    p.grad_f32 = 1;
+  }
 
   if ((e = launch_bwd_preprocess(p, stream)) != hipSuccess) return hip_fail(e, "preprocess launch");
   if ((e = record(io->ring_begin, stream)) != hipSuccess) return hip_fail(e, "event record");
@@ -265,6 +340,26 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
   }
   if (has_br) {
     if ((e = launch_bwd_branch(p, P.max_group_len, stream)) != hipSuccess) return hip_fail(e, "branch backward launch");
+  }
+  if (rope) {
+    // gradients with respect to the unrotated queries and keys: the
+    // transposed rotation of the staged ones (values were not rotated)
+    const RopeTables rt = rope_tables(P, c);
+    const bool f32 = io->grad_dtype == BA_DTYPE_F32;
+    const int64_t nl = P.n_local, nb = P.num_branch_rows;
+    auto grad = [&](const void* src, void* dst, const int32_t* pos, int64_t rows, int heads, bool rot) {
+      return launch_rope_grad(static_cast<const float*>(src), dst, f32, pos, rt.freq, rows, heads, rot, stream);
+    };
+    if (has_main && (e = grad(p.dq_main, io->dq_main, rt.pos_qmain, nl, P.hq, true)))
+      return hip_fail(e, "rotary gradient launch");
+    if (has_br && ((e = grad(p.dq_br, io->dq_br, rt.pos_br, nb, P.hq, true)) ||
+                   (e = grad(p.dk_br, io->dk_br, rt.pos_br, nb, P.hkv, true)) ||
+                   (e = grad(p.dv_br, io->dv_br, rt.pos_br, nb, P.hkv, false))))
+      return hip_fail(e, "rotary gradient launch");
+    for (int j = 0; j < P.cp_size && has_keys; ++j)
+      if ((e = grad(p.dk_step[j], io->dk_step[j], rt.pos_block + j * nl, nl, P.hkv, true)) ||
+          (e = grad(p.dv_step[j], io->dv_step[j], rt.pos_block + j * nl, nl, P.hkv, false)))
+        return hip_fail(e, "rotary gradient launch");
   }
   return BA_OK;
 }

@@ -53,7 +53,14 @@ struct GroupInfo {
   int32_t len;
   int32_t kind;
   int32_t tok0;  // token-table index of member 0 (members are consecutive)
-  int32_t pad[3];
+  int32_t anchor;
+  int32_t pad[2];
+};
+
+// Rotary embedding frequency of dim pair j: theta^(-j/64) / (2 pi) turns per
+// position, as an unevaluated float sum hi + lo.
+struct RopeFreq {
+  float hi, lo;
 };
 
 struct FwdTile {
@@ -103,6 +110,17 @@ struct Plan {
   // packed image of the tables and their byte offsets inside it
   std::vector<uint8_t> image;
   size_t off_seqs = 0, off_toks = 0, off_groups = 0, off_fwd = 0, off_bwd = 0;
+  // rotary position embedding (off while rope_theta == 0): positions of the
+  // rows of every ring-step block ([C][n_local], block j = rank j's local
+  // rows), of this rank's main rows that are queries and of the branch rows
+  // in a group (-1 elsewhere: such rows are neither read nor written), and
+  // the frequency table
+  float rope_theta = 0.f;
+  std::vector<int32_t> pos_block;
+  std::vector<int32_t> pos_qmain;
+  std::vector<int32_t> pos_br;
+  std::vector<RopeFreq> rope_freq;
+  size_t off_pos_block = 0, off_pos_qmain = 0, off_pos_br = 0, off_freq = 0;
   // counts
   double pairs_per_head = 0.0;  // allowed (query, key) pairs per query head
   double main_pairs_per_head = 0.0;   // ... of which on the causal main prefix
@@ -118,11 +136,18 @@ struct WorkspaceLayout {
   size_t qtok = 0;     // bf16 [T, hq, d]   (backward: Q in token order)
   size_t gtok = 0;     // bf16 [T, hq, d]   (backward: dO in token order)
   size_t dq_acc = 0;   // fp32 [T, hq, d]   (backward)
+  // rotary embedding: rotated bf16 copies of the inputs (both passes) and
+  // fp32 staging of the gradients (backward)
+  size_t rq_main = 0, rq_br = 0, rk_step = 0, rk_br = 0;
+  size_t gq_main = 0, gq_br = 0, gk_step = 0, gv_step = 0, gk_br = 0, gv_br = 0;
   size_t fwd_total = 0;
   size_t bwd_total = 0;
 };
 
 WorkspaceLayout workspace_layout(const Plan& p, int mode);
+
+// (re)build the packed table image of a plan
+void pack_image(Plan& P);
 
 // thread-local error message
 void set_error(const std::string& msg);

@@ -927,7 +927,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
     }
     // ---- branch-local keys of this row (vector ALUs)
     int nb = 0;
-    GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
+    GroupInfo gi{0, 1, 0, 0, 0, 0, {0, 0}};
     if (valid[rb] && tk[rb].grp >= 0) {
       gi = p.groups[tk[rb].grp];
       nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk[rb].gidx + 1 : gi.len;
@@ -1007,7 +1007,7 @@ __global__ __launch_bounds__(256) void bwd_dq_finalize_kernel(BwdParams p) {
   float acc[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
 
   int nb = 0;
-  GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
+  GroupInfo gi{0, 1, 0, 0, 0, 0, {0, 0}};
   if (tk.grp >= 0) {
     gi = p.groups[tk.grp];
     nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk.gidx + 1 : gi.len;

@@ -409,7 +409,7 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
 
     // ---- branch-local partial (vector ALUs; at most 64 keys per row)
     int nb = 0;
-    GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
+    GroupInfo gi{0, 1, 0, 0, 0, 0, {0, 0}};
     if (valid[rb] && tk[rb].grp >= 0) {
       gi = p.groups[tk[rb].grp];
       nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk[rb].gidx + 1 : gi.len;
@@ -512,7 +512,7 @@ __global__ __launch_bounds__(256) void fwd_finalize_kernel(FwdParams p) {
   const float lse_m = p.lse_acc[R];  // log2 units; -inf: no main key
 
   int nb = 0;
-  GroupInfo gi{0, 1, 0, 0, 0, {0, 0, 0}};
+  GroupInfo gi{0, 1, 0, 0, 0, 0, {0, 0}};
   if (tk.grp >= 0) {
     gi = p.groups[tk.grp];
     nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk.gidx + 1 : gi.len;

@@ -43,10 +43,23 @@ WorkspaceLayout workspace_layout(const Plan& p, int mode) {
   WorkspaceLayout w;
   size_t T = p.toks.size();
   size_t rows = T * (size_t)p.hq;
+  const bool rope = p.rope_theta > 0.f;
+  const size_t nl = (size_t)p.n_local, nb = (size_t)p.num_branch_rows, C = (size_t)p.cp_size;
+  const size_t qrow = (size_t)p.hq * kHeadDim, krow = (size_t)p.hkv * kHeadDim;
   size_t off = 0;
   w.tables = off;
   off = align(off + p.image.size());
-  size_t after_tables = off;
+  if (rope) {  // rotated inputs, shared by the forward and backward layouts
+    w.rq_main = off;
+    off = align(off + nl * qrow * sizeof(uint16_t));
+    w.rq_br = off;
+    off = align(off + nb * qrow * sizeof(uint16_t));
+    w.rk_step = off;
+    off = align(off + C * nl * krow * sizeof(uint16_t));
+    w.rk_br = off;
+    off = align(off + nb * krow * sizeof(uint16_t));
+  }
+  const size_t common = off;
   if (mode == BA_MODE_PER_STEP) {
     w.o_acc = off;
     off = align(off + rows * kHeadDim * sizeof(float));
@@ -54,7 +67,7 @@ WorkspaceLayout workspace_layout(const Plan& p, int mode) {
     off = align(off + rows * sizeof(float));
   }
   w.fwd_total = off;
-  off = after_tables;
+  off = common;
   w.rowstat = off;
   off = align(off + rows * 2 * sizeof(float));
   w.qtok = off;
@@ -64,6 +77,20 @@ WorkspaceLayout workspace_layout(const Plan& p, int mode) {
   if (mode == BA_MODE_PER_STEP) {
     w.dq_acc = off;
     off = align(off + rows * kHeadDim * sizeof(float));
+  }
+  if (rope) {
+    w.gq_main = off;
+    off = align(off + nl * qrow * sizeof(float));
+    w.gq_br = off;
+    off = align(off + nb * qrow * sizeof(float));
+    w.gk_step = off;
+    off = align(off + C * nl * krow * sizeof(float));
+    w.gv_step = off;
+    off = align(off + C * nl * krow * sizeof(float));
+    w.gk_br = off;
+    off = align(off + nb * krow * sizeof(float));
+    w.gv_br = off;
+    off = align(off + nb * krow * sizeof(float));
   }
   w.bwd_total = off;
   return w;
@@ -134,7 +161,7 @@ static int build_plan(const ba_problem* pr, Plan& P) {
   P.groups.resize(pr->num_groups);
   for (int32_t g = 0; g < pr->num_groups; ++g) {
     P.groups[g] = GroupInfo{pr->groups[g].row0, pr->groups[g].row_stride, pr->groups[g].len,
-                            pr->groups[g].kind, -1, {0, 0, 0}};
+                            pr->groups[g].kind, -1, pr->groups[g].anchor, {0, 0}};
     P.max_group_len = std::max(P.max_group_len, pr->groups[g].len);
   }
 
@@ -242,7 +269,11 @@ static int build_plan(const ba_problem* pr, Plan& P) {
     P.bwd_step_off[i + 1] = (int32_t)P.bwd_tiles.size();
   }
 
-  // --- packed table image
+  pack_image(P);
+  return BA_OK;
+}
+
+void pack_image(Plan& P) {
   P.image.clear();
   P.off_seqs = append(P.image, P.seqs);
   // the token table is followed by a sentinel whose causal limit -1 admits
@@ -253,7 +284,64 @@ static int build_plan(const ba_problem* pr, Plan& P) {
   P.off_groups = append(P.image, P.groups);
   P.off_fwd = append(P.image, P.fwd_tiles);
   P.off_bwd = append(P.image, P.bwd_tiles);
+  if (P.rope_theta > 0.f) {
+    P.off_pos_block = append(P.image, P.pos_block);
+    P.off_pos_qmain = append(P.image, P.pos_qmain);
+    P.off_pos_br = append(P.image, P.pos_br);
+    P.off_freq = append(P.image, P.rope_freq);
+  }
   P.image.resize((P.image.size() + 255) & ~size_t(255));
+}
+
+// Rotary embedding tables: the position of every row of every ring-step
+// block (rank j's local order: chunk j, then chunk 2C-1-j of each sequence)
+// and of every branch row (anchor + 1 + member index), and the frequency of
+// each of the 64 dim pairs in turns per position.
+static int build_rope(Plan& P, float theta) {
+  if (!std::isfinite(theta) || theta < 0.f) return fail(BA_E_INVAL, "rope theta must be finite and >= 0");
+  P.rope_theta = theta;
+  P.pos_block.clear();
+  P.pos_qmain.clear();
+  P.pos_br.clear();
+  P.rope_freq.clear();
+  if (theta > 0.f) {
+    const int32_t C = P.cp_size;
+    int64_t max_pos = 0;
+    P.pos_block.resize((size_t)C * P.n_local);
+    for (int32_t j = 0; j < C; ++j)
+      for (int32_t s = 0; s < P.num_seqs; ++s) {
+        const SeqInfo& si = P.seqs[s];
+        for (int32_t u = 0; u < 2 * si.c; ++u) {
+          const int32_t pos = u < si.c ? j * si.c + u : (2 * C - 1 - j) * si.c + (u - si.c);
+          P.pos_block[(size_t)j * P.n_local + si.seg_off + u] = pos;
+          max_pos = std::max<int64_t>(max_pos, pos);
+        }
+      }
+    P.pos_qmain.assign((size_t)P.n_local, -1);
+    for (const TokInfo& t : P.toks)
+      if (t.qrow >= 0) P.pos_qmain[t.qrow] = P.pos_block[(size_t)P.cp_rank * P.n_local + t.qrow];
+    P.pos_br.assign((size_t)P.num_branch_rows, -1);
+    for (const GroupInfo& g : P.groups)
+      for (int32_t i = 0; i < g.len; ++i) {
+        P.pos_br[(size_t)g.row0 + (size_t)i * g.stride] = g.anchor + 1 + i;
+        max_pos = std::max<int64_t>(max_pos, (int64_t)g.anchor + 1 + i);
+      }
+    if (max_pos >= (1 << 24)) {
+      P.rope_theta = 0.f;
+      P.pos_block.clear();
+      P.pos_qmain.clear();
+      P.pos_br.clear();
+      pack_image(P);
+      return fail(BA_E_UNSUPPORTED, "rope positions must stay below 2^24");
+    }
+    const double two_pi = 6.283185307179586476925286766559;
+    for (int j = 0; j < kHeadDim / 2; ++j) {
+      const double f = std::pow((double)theta, -(double)j / (kHeadDim / 2)) / two_pi;
+      const float hi = (float)f;
+      P.rope_freq.push_back(RopeFreq{hi, (float)(f - (double)hi)});
+    }
+  }
+  pack_image(P);
   return BA_OK;
 }
 
@@ -310,6 +398,15 @@ int branch_attn_plan_create(const ba_problem* prob, ba_plan** out) {
 }
 
 void branch_attn_plan_destroy(ba_plan* plan) { delete plan; }
+
+int branch_attn_plan_set_rope(ba_plan* plan, float theta) {
+  if (!plan) return ba::fail(BA_E_INVAL, "plan is NULL");
+  try {
+    return ba::build_rope(plan->p, theta);
+  } catch (const std::exception& e) {
+    return ba::fail(BA_E_INVAL, std::string("rope tables: ") + e.what());
+  }
+}
 
 int branch_attn_workspace_size(const ba_plan* plan, int32_t mode, size_t* fwd_bytes, size_t* bwd_bytes) {
   if (!plan) return ba::fail(BA_E_INVAL, "plan is NULL");

@@ -88,7 +88,7 @@ def _layout_groups(prob: GlobalProblem, r: int, l2g: np.ndarray, layout: str):
 
 def build_share(prob: GlobalProblem, device: str = "cuda", layout: str = "group",
                 with_grad: Optional[bool] = None, zero_q: bool = False,
-                materialize: bool = True) -> RankShare:
+                materialize: bool = True, rope_theta: float = 0.0) -> RankShare:
     C, r = prob.cp_size, prob.cp_rank
     cu = prob.cu_seqlens.astype(np.int32)
     lcu, l2g, lpos = B.zigzag_partition(cu, C, r)
@@ -97,6 +97,8 @@ def build_share(prob: GlobalProblem, device: str = "cuda", layout: str = "group"
     desc, gsel, loc_rows, glob_rows, nrows = _layout_groups(prob, r, l2g, layout)
     plan = B.Plan(cu, prob.has_main.astype(np.uint8), C, r, prob.hq, prob.hkv, prob.head_dim,
                   prob.scale, desc, nrows)
+    if rope_theta:
+        plan.set_rope(rope_theta)
     seq_of_local = np.searchsorted(lcu, np.arange(n_local), side="right") - 1
     mq_rows = np.flatnonzero(prob.has_main[seq_of_local]) if n_local else np.zeros(0, np.int64)
     share = RankShare(prob=prob, plan=plan, n_local=n_local, local_cu=lcu, l2g=l2g, l2g_steps=l2g_steps,

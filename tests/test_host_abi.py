@@ -139,3 +139,36 @@ def test_workspace_sizes():
     # per-step backward keeps running fp32 dQ sums; the fused one needs only row statistics
     assert b_step >= ntok * prob.hq * (128 + 2) * 4
     assert ntok * prob.hq * 2 * 4 <= b_fused < b_step
+
+
+def test_rope_settings():
+    prob = W.config(1)
+    share = RS.build_share(prob, materialize=False)
+    plain = share.plan.workspace_size(B.BA_MODE_PER_STEP)
+    for bad in (-1.0, float("nan"), float("inf")):
+        with pytest.raises(B.BranchAttnError) as e:
+            share.plan.set_rope(bad)
+        assert e.value.code == B.BA_E_INVAL
+    share.plan.set_rope(1.0e4)
+    n_local, _ = share.plan.info()
+    rot = share.plan.workspace_size(B.BA_MODE_PER_STEP)
+    # rotated bf16 copies of Q and the C key blocks in both passes, fp32
+    # gradient staging (dQ, dK, dV) in the backward
+    C, hq, hkv, nb = prob.cp_size, prob.hq, prob.hkv, share.num_branch_rows
+    copies = 2 * 128 * ((n_local + nb) * hq + (C * n_local + nb) * hkv)
+    assert rot[0] - plain[0] >= copies
+    assert rot[1] - plain[1] >= copies + 4 * 128 * ((n_local + nb) * hq + 2 * (C * n_local + nb) * hkv)
+    share.plan.set_rope(0.0)
+    assert share.plan.workspace_size(B.BA_MODE_PER_STEP) == plain
+
+
+def test_rope_positions_must_fit_float():
+    # one sequence of 2^24 tokens with a branch anchored at its last token:
+    # the branch member's position 2^24 is not exact in float32
+    L = 1 << 24
+    plan = B.Plan([0, L], [1], 8, 0, 1, 1, 128, 0.088, np.array([[0, L - 1, 0, 1, 0, 1]], np.int32), 1)
+    before = plan.workspace_size(B.BA_MODE_PER_STEP)
+    with pytest.raises(B.BranchAttnError) as e:
+        plan.set_rope(1.0e4)
+    assert e.value.code == B.BA_E_UNSUPPORTED
+    assert plan.workspace_size(B.BA_MODE_PER_STEP) == before  # left without rotation

@@ -6,7 +6,8 @@ and `apply_rotary_pos_emb`, a library special case), R2 the relative-position
 identity that defines rotary embeddings, R3 orthogonality and the inverse,
 R4 shift invariance of the whole attention output, R5 central finite
 differences through rotation + attention (pins the transposed rotation of
-the gradients).
+the gradients), R6 the bfloat16 rounding of the rotated operands against
+torch's float32 -> bfloat16 conversion.
 """
 
 import numpy as np
@@ -145,3 +146,18 @@ def test_r5_finite_differences_through_rotation():
             fd = (lp - lm) / (2 * h)
             an = g[grad_name][gi, hh, dd]
             assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, row, hh, dd, fd, an)
+
+
+def test_r6_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(78)
+    x = np.r_[rng.standard_normal(20000) * np.exp(rng.uniform(-20, 20, 20000)), 0.0, -0.0, 1.0, -3.0]
+    # exact ties: a bfloat16 value plus half of its last place (float32-representable)
+    b = torch.from_numpy(rng.standard_normal(4000).astype(np.float32)).to(torch.bfloat16).float().numpy()
+    _, e = np.frexp(b)
+    x = np.r_[x, b + np.ldexp(1.0, e - 9)]
+    x32 = x.astype(np.float32)  # float32 inputs: torch's conversion rounds once, ties to even
+    ref = torch.from_numpy(x32).to(torch.bfloat16).float().numpy().astype(np.float64)
+    got = rope.round_bf16(x32.astype(np.float64))
+    assert np.array_equal(got, ref)
+    t = np.array([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, -(1.0 + 2.0 ** -8)])
+    assert list(rope.round_bf16(t)) == [1.0, 1.0 + 2.0 ** -6, -1.0]
