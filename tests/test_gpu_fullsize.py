@@ -31,7 +31,11 @@ from tests import gpu_helpers as H
 
 pytestmark = pytest.mark.gpu
 
-CASES = [(2, "per_step"), (3, "fused"), (4, "fused"), (5, "fused")]
+# (config, schedule, sampled main rows, sampled branch rows); the headline
+# share (config 4) runs in both schedules, the per-step one being the
+# benchmark's launch configuration
+CASES = [(2, "per_step", 4, 8), (3, "fused", 4, 8), (4, "per_step", 12, 24), (4, "fused", 4, 8),
+         (5, "fused", 4, 8)]
 
 
 def sample_rows(prob, mq, bq, n_main=4, n_br=8, seed=0):
@@ -52,8 +56,8 @@ def cuda():
     return torch.device("cuda:0")
 
 
-@pytest.mark.parametrize("cfg,mode", CASES)
-def test_fullsize_sampled_rows_and_gradient_identities(cuda, cfg, mode):
+@pytest.mark.parametrize("cfg,mode,n_main,n_br", CASES)
+def test_fullsize_sampled_rows_and_gradient_identities(cuda, cfg, mode, n_main, n_br):
     prob = W.config(cfg)
     md = B.BA_MODE_FUSED if mode == "fused" else B.BA_MODE_PER_STEP
     share = RS.build_share(prob, device="cuda:0", with_grad=True)
@@ -66,7 +70,7 @@ def test_fullsize_sampled_rows_and_gradient_identities(cuda, cfg, mode):
 
     # ---- sampled rows against the oracle
     mq, bq = oracle.select_queries(prob)
-    sm, sb = sample_rows(prob, mq, bq, seed=cfg)
+    sm, sb = sample_rows(prob, mq, bq, n_main=n_main, n_br=n_br, seed=cfg)
     H_, Hk, d = prob.hq, prob.hkv, prob.head_dim
 
     def sparse(name, sel, total, heads):
@@ -127,4 +131,79 @@ def test_fullsize_sampled_rows_and_gradient_identities(cuda, cfg, mode):
           f"<dQ,Q>=<dK,K> {e3.item():.2e}", flush=True)
     assert e1 <= 5e-3, f"sum_k dV_k != sum dO: {e1.item():.3e}"
     assert e2 <= 2e-2, f"sum_k dK_k != 0: {e2.item():.3e}"
+    assert e3 <= 1e-2, f"<dQ,Q> != <dK,K>: {e3.item():.3e}"
+
+
+def test_fullsize_headline_with_rotary_embedding(cuda):
+    """The headline share with rotary embedding (theta 5e5, positions up to
+    262143, so angles of ~2.6e5 rad): sampled rows against `oracle.rope`
+    (rotated queries and keys rounded to bf16), plus the two identities that
+    survive the rotation: sum_k dV_k = sum dO (values are not rotated) and
+    sum_q <dQ_q, q_q> = sum_k <dK_k, k_k> (the rotation is orthogonal)."""
+    from oracle import rope
+
+    theta = 5.0e5
+    prob = W.config(4)
+    md = B.BA_MODE_PER_STEP
+    share = RS.build_share(prob, device="cuda:0", with_grad=True, rope_theta=theta)
+    out = RS.alloc_outputs(share, grads=True, grad_dtype=torch.float32)
+    ws = RS.workspace(share, md, backward=True)
+    RS.run_fwd(share, out, md, ws)
+    RS.run_bwd(share, out, md, ws)
+    torch.cuda.synchronize()
+    print("[fullsize] config 4 with rotary embedding: GPU done", flush=True)
+
+    mq, bq = oracle.select_queries(prob)
+    sm, sb = sample_rows(prob, mq, bq, n_main=6, n_br=12, seed=44)
+    H_, Hk, d = prob.hq, prob.hkv, prob.head_dim
+
+    def sparse(name, sel, total, heads):
+        a = np.zeros((total, heads, d), np.float32)
+        if len(sel):
+            a[sel] = prob.draw(name, sel).float().numpy()
+        return a
+
+    grp = np.repeat(np.arange(len(prob.g_len)), prob.g_len)
+    gsel = np.unique(grp[sb]) if len(sb) else np.zeros(0, np.int64)
+    brows = np.concatenate([np.arange(prob.g_row0[g], prob.g_row0[g] + prob.g_len[g]) for g in gsel]) \
+        if len(gsel) else np.zeros(0, np.int64)
+    t = dict(qm=sparse("qm", sm, prob.n_main, H_), qb=sparse("qb", sb, prob.n_branch, H_),
+             km=prob.draw("km").float().numpy(), vm=prob.draw("vm").float().numpy(),
+             kb=sparse("kb", brows, prob.n_branch, Hk), vb=sparse("vb", brows, prob.n_branch, Hk))
+    args = [t[k] for k in ("qm", "km", "vm", "qb", "kb", "vb")]
+    ref_f = rope.forward(prob, *args, theta, rounded=True, main_q=sm, br_q=sb)
+    dom = prob.draw("dom", sm).float().numpy()
+    dob = prob.draw("dob", sb).float().numpy()
+    ref_b = rope.backward(prob, *args, dom, dob, theta, main_q=sm, br_q=sb, rounded=True)
+    print(f"[fullsize] rotary oracle done on {len(sm)} main + {len(sb)} branch rows", flush=True)
+
+    g2l = {int(g): i for i, g in enumerate(share.l2g)}
+    mi = np.array([g2l[int(g)] for g in sm], np.int64)
+    bmap = {int(g): int(l) for g, l in zip(share.br_rows_global, share.br_rows_local)}
+    bi = np.array([bmap[int(g)] for g in sb], np.int64)
+    f = lambda x, idx: x[torch.from_numpy(idx).to(x.device)].float().cpu().numpy().astype(np.float64)
+    got_f = (f(out["o_main"], mi), f(out["lse_main"].T, mi).T, f(out["o_br"], bi), f(out["lse_br"].T, bi).T)
+    H.assert_fwd_close(got_f, ref_f)
+    dq = np.concatenate([f(out["dq_main"], mi).ravel(), f(out["dq_br"], bi).ravel()])
+    dq_ref = np.concatenate([ref_b["dq_main"].ravel(), ref_b["dq_br"].ravel()])
+    e = H.rel_l2(dq, dq_ref)
+    assert e <= H.GRAD_TOL, f"sampled dQ rows: relative L2 {e:.3e}"
+
+    G = H_ // Hk
+    dev = cuda
+    mrows = torch.from_numpy(share.main_query_rows).to(dev)
+    br_idx = torch.from_numpy(share.br_rows_local).to(dev)
+    q_rows = torch.cat([share.t["q_main"][mrows], share.t["q_br"][br_idx]]).double()
+    do_rows = torch.cat([share.t["do_main"][mrows], share.t["do_br"][br_idx]]).double()
+    dq_rows = torch.cat([out["dq_main"][mrows], out["dq_br"][br_idx]]).double()
+    dk_all = torch.cat([x.double() for x in out["dk_step"]] + [out["dk_br"][br_idx].double()])
+    dv_all = torch.cat([x.double() for x in out["dv_step"]] + [out["dv_br"][br_idx].double()])
+    k_all = torch.cat([x.double() for x in share.t["k_step"]] + [share.t["k_br"][br_idx].double()])
+    sum_do = do_rows.view(-1, Hk, G, d).sum((0, 2))
+    e1 = (dv_all.sum(0) - sum_do).norm() / sum_do.norm()
+    lhs = (dq_rows * q_rows).view(-1, Hk, G, d).sum((0, 2, 3))
+    rhs = (dk_all * k_all).sum((0, 2))
+    e3 = ((lhs - rhs).abs() / (dq_rows * q_rows).abs().view(-1, Hk, G, d).sum((0, 2, 3))).max()
+    print(f"[fullsize] rotary identities: dV sum {e1.item():.2e}, <dQ,Q>=<dK,K> {e3.item():.2e}", flush=True)
+    assert e1 <= 5e-3, f"sum_k dV_k != sum dO: {e1.item():.3e}"
     assert e3 <= 1e-2, f"<dQ,Q> != <dK,K>: {e3.item():.3e}"
