@@ -296,6 +296,9 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
   p.qtok = reinterpret_cast<bf16*>(c.ws + c.w.qtok);
   p.gtok = reinterpret_cast<bf16*>(c.ws + c.w.gtok);
   p.dq_acc = mode == BA_MODE_PER_STEP ? reinterpret_cast<float*>(c.ws + c.w.dq_acc) : nullptr;
+  p.kv_part = P.kv_slots > 0 ? reinterpret_cast<float*>(c.ws + c.w.kv_part) : nullptr;
+  p.splits = reinterpret_cast<const KvSplit*>(c.ws + c.w.tables + P.off_splits);
+  p.num_splits = (int32_t)P.kv_splits.size();
   if (rope) {
     if ((e = rotate_inputs(P, c, io->q_main, io->q_br, io->k_br, io->k_step, has_main, has_br, has_keys, p, stream)))
       return hip_fail(e, "rotary embedding launch");
@@ -313,6 +316,7 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
     p.tiles = tiles;
     p.num_tiles = (int32_t)P.bwd_tiles.size();
     if ((e = launch_bwd_kv(p, stream)) != hipSuccess) return hip_fail(e, "dK/dV launch");
+    if ((e = launch_bwd_kv_reduce(p, stream)) != hipSuccess) return hip_fail(e, "dK/dV partial-sum launch");
     if ((e = record(io->kv_end, stream)) != hipSuccess) return hip_fail(e, "event record");
     p.step_first = 0;
     p.step_count = P.cp_size;
@@ -328,6 +332,7 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
       p.num_tiles = P.bwd_step_off[i + 1] - P.bwd_step_off[i];
       if ((e = launch_bwd_kv(p, stream)) != hipSuccess) return hip_fail(e, "ring-step dK/dV launch");
     }
+    if ((e = launch_bwd_kv_reduce(p, stream)) != hipSuccess) return hip_fail(e, "dK/dV partial-sum launch");
     if ((e = record(io->kv_end, stream)) != hipSuccess) return hip_fail(e, "event record");
     for (int i = 0; i < P.cp_size; ++i) {
       p.step_first = i;

@@ -76,10 +76,32 @@ struct BwdTile {
   int32_t kvh;
   int32_t u0;       // first key, as an index inside the sequence's segment
   int32_t nk;       // keys in this item (<= kBwdKeys)
-  int32_t q_begin;  // first token that sees at least one of the keys
+  int32_t q_begin;  // first token of the item that sees at least one of the keys
   int32_t q_full;   // tokens >= q_full see all of them
   int32_t q_end;
+  int32_t slot;     // -1: the item writes dK, dV; else its fp32 partial slot
+  int32_t pad[3];
 };
+
+// Keys whose query range was split into several work items: the items'
+// fp32 partial dK, dV (slots slot0 .. slot0 + nslots - 1) are summed into
+// the outputs afterwards.
+struct KvSplit {
+  int32_t step;
+  int32_t key0;  // first key row in block `step` (segment offset + u0)
+  int32_t kvh;
+  int32_t nk;
+  int32_t slot0;
+  int32_t nslots;
+  int32_t pad[2];
+};
+
+// A ring step whose backward work items number fewer than this has its
+// longest items split along the query range, so one launch still fills the
+// GPU (four items per compute unit of an MI355X).
+constexpr int32_t kKvSplitBelow = 1024;
+// smallest piece of a split item, in 64-row query tiles
+constexpr int32_t kKvSplitMinTiles = 16;
 
 // Number of keys of ring-step block j (rank j's chunks j and 2C-1-j of a
 // sequence with chunk length c) at positions <= P.  Positions increase with
@@ -107,9 +129,11 @@ struct Plan {
   std::vector<FwdTile> fwd_tiles;
   std::vector<BwdTile> bwd_tiles;      // grouped by ring step i = 0..C-1
   std::vector<int32_t> bwd_step_off;   // [C+1] tile range of each ring step
+  std::vector<KvSplit> kv_splits;      // keys whose items write partial sums
+  int32_t kv_slots = 0;                // partial slots in use
   // packed image of the tables and their byte offsets inside it
   std::vector<uint8_t> image;
-  size_t off_seqs = 0, off_toks = 0, off_groups = 0, off_fwd = 0, off_bwd = 0;
+  size_t off_seqs = 0, off_toks = 0, off_groups = 0, off_fwd = 0, off_bwd = 0, off_splits = 0;
   // rotary position embedding (off while rope_theta == 0): positions of the
   // rows of every ring-step block ([C][n_local], block j = rank j's local
   // rows), of this rank's main rows that are queries and of the branch rows
@@ -136,6 +160,7 @@ struct WorkspaceLayout {
   size_t qtok = 0;     // bf16 [T, hq, d]   (backward: Q in token order)
   size_t gtok = 0;     // bf16 [T, hq, d]   (backward: dO in token order)
   size_t dq_acc = 0;   // fp32 [T, hq, d]   (backward)
+  size_t kv_part = 0;  // fp32 [slots][dV, dK][kBwdKeys][d] (backward, split items)
   // rotary embedding: rotated bf16 copies of the inputs (both passes) and
   // fp32 staging of the gradients (backward)
   size_t rq_main = 0, rq_br = 0, rk_step = 0, rk_br = 0;

@@ -570,9 +570,23 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
     for (int nt = 0; nt < 4; ++nt) acc_settle(acc[kb][nt]);  // the reads below stay after the drain
 
   // ---- write dV (score side) or dK (gradient side, scaled): accumulator
-  // column = dim, rows = keys
-  void* out = scorer ? p.dv_step[tile.step] : p.dk_step[tile.step];
+  // column = dim, rows = keys; an item covering part of its keys' query
+  // range writes an fp32 partial sum into its slot instead
   const float mul = scorer ? 1.f : p.scale;
+  if (tile.slot >= 0) {
+    float* part = p.kv_part + ((int64_t)tile.slot * 2 + (scorer ? 0 : 1)) * (kBwdKeys * kHeadDim);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = 64 * pair + 32 * kb + 8 * (v >> 2) + 4 * half + (v & 3);
+          part[key * kHeadDim + 32 * nt + qi] = acc[kb][nt][v] * mul;
+        }
+    return;
+  }
+  void* out = scorer ? p.dv_step[tile.step] : p.dk_step[tile.step];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -585,6 +599,32 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
           store_grad(out, idx, acc[kb][nt][v] * mul, p.grad_f32);
         }
       }
+}
+
+// Sum of the fp32 partial dV, dK of a split work item's pieces into the
+// outputs (one workgroup per split key range; the pieces' slots are
+// consecutive).  Keys past nk hold partial sums of clamped copies and are
+// not written.
+__global__ __launch_bounds__(256) void bwd_kv_reduce_kernel(BwdParams p) {
+  const KvSplit sp = p.splits[blockIdx.x];
+  const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
+  constexpr int kPerSide = kBwdKeys * kHeadDim;
+  for (int i = threadIdx.x * 4; i < 2 * kPerSide; i += blockDim.x * 4) {
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s = 0; s < sp.nslots; ++s) {
+      const float4 b = *reinterpret_cast<const float4*>(p.kv_part + (int64_t)(sp.slot0 + s) * 2 * kPerSide + i);
+      a.x += b.x;
+      a.y += b.y;
+      a.z += b.z;
+      a.w += b.w;
+    }
+    const int side = i / kPerSide, key = (i % kPerSide) / kHeadDim, d = i % kHeadDim;
+    if (key >= sp.nk) continue;
+    void* out = side == 0 ? p.dv_step[sp.step] : p.dk_step[sp.step];
+    const int64_t idx = (int64_t)(sp.key0 + key) * kv_row_stride + sp.kvh * kHeadDim + d;
+    if (p.grad_f32) *reinterpret_cast<float4*>(static_cast<float*>(out) + idx) = a;
+    else *reinterpret_cast<bf16x4*>(static_cast<bf16*>(out) + idx) = pack4(a.x, a.y, a.z, a.w);
+  }
 }
 
 // ------------------------------------------------------------ dq
@@ -1190,6 +1230,12 @@ hipError_t launch_bwd_dq(const BwdParams& p, int mode, hipStream_t stream) {
   dim3 grid(p.num_qtiles), block(256);
   if (mode == kModeStep) hipLaunchKernelGGL(bwd_dq_kernel<kModeStep>, grid, block, 0, stream, p);
   else hipLaunchKernelGGL(bwd_dq_kernel<kModeFused>, grid, block, 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_kv_reduce(const BwdParams& p, hipStream_t stream) {
+  if (p.num_splits == 0) return hipSuccess;
+  hipLaunchKernelGGL(bwd_kv_reduce_kernel, dim3(p.num_splits), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 

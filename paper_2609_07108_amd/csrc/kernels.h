@@ -77,6 +77,9 @@ struct BwdParams {
   bf16* qtok;       // [T * hq, d] Q rows in token order (written by the preprocess)
   bf16* gtok;       // [T * hq, d] dO rows in token order
   float* dq_acc;    // [T * hq, d] running unscaled dS K sums (per-step schedule)
+  float* kv_part;   // [slots][dV, dK][kBwdKeys][d] partial sums of split work items
+  const KvSplit* splits;
+  int32_t num_splits;
 };
 
 // Cursor of a walk over (ring step i, block j = (rank - i) mod C, first key
@@ -92,6 +95,7 @@ hipError_t launch_bwd_kv(const BwdParams& p, hipStream_t stream);
 hipError_t launch_bwd_dq(const BwdParams& p, int mode, hipStream_t stream);
 hipError_t launch_bwd_dq_finalize(const BwdParams& p, hipStream_t stream);
 hipError_t launch_bwd_branch(const BwdParams& p, int max_group_len, hipStream_t stream);
+hipError_t launch_bwd_kv_reduce(const BwdParams& p, hipStream_t stream);
 hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t stream);
 // rotary embedding of bf16 rows [rows, heads, 128] (positions < 0: row skipped)
 hipError_t launch_rope_rows(const bf16* src, bf16* dst, const int32_t* pos, const RopeFreq* freq, int64_t rows,

@@ -78,6 +78,10 @@ WorkspaceLayout workspace_layout(const Plan& p, int mode) {
     w.dq_acc = off;
     off = align(off + rows * kHeadDim * sizeof(float));
   }
+  if (p.kv_slots > 0) {
+    w.kv_part = off;
+    off = align(off + (size_t)p.kv_slots * 2 * kBwdKeys * kHeadDim * sizeof(float));
+  }
   if (rope) {
     w.gq_main = off;
     off = align(off + nl * qrow * sizeof(float));
@@ -261,8 +265,40 @@ static int build_plan(const ba_problem* pr, Plan& P) {
         const int32_t qf = first_with(u0 + nk);
         if (qb == si.tok_end) continue;
         for (int32_t h = 0; h < pr->hkv; ++h)
-          bt.push_back(KeyedB{(int64_t)(si.tok_end - qb), BwdTile{j, s, h, u0, nk, qb, qf, si.tok_end}});
+          bt.push_back(KeyedB{(int64_t)(si.tok_end - qb),
+                              BwdTile{j, s, h, u0, nk, qb, qf, si.tok_end, -1, {0, 0, 0}}});
       }
+    }
+    // few items: split the longest along their query range (whole 64-row
+    // query tiles per piece) into pieces of about total / kKvSplitBelow
+    if (!bt.empty() && (int32_t)bt.size() < kKvSplitBelow) {
+      const int32_t qt = kBwdRows / G;  // tokens per 64-row query tile
+      int64_t total = 0;
+      for (const auto& k : bt) total += (k.t.q_end - k.t.q_begin + qt - 1) / qt;
+      const int64_t piece = std::max<int64_t>(kKvSplitMinTiles, (total + kKvSplitBelow - 1) / kKvSplitBelow);
+      std::vector<KeyedB> split;
+      for (const auto& k : bt) {
+        const int64_t nt = (k.t.q_end - k.t.q_begin + qt - 1) / qt;
+        const int64_t parts = (nt + piece - 1) / piece;
+        if (parts < 2) {
+          split.push_back(k);
+          continue;
+        }
+        const int32_t slot0 = P.kv_slots;
+        const int32_t seg_off = P.seqs[k.t.seq].seg_off;
+        P.kv_splits.push_back(KvSplit{k.t.step, seg_off + k.t.u0, k.t.kvh, k.t.nk, slot0, (int32_t)parts, {0, 0}});
+        P.kv_slots += (int32_t)parts;
+        for (int64_t q = 0; q < parts; ++q) {
+          BwdTile t = k.t;
+          const int64_t t0 = q * nt / parts, t1 = (q + 1) * nt / parts;
+          t.q_begin = k.t.q_begin + (int32_t)(t0 * qt);
+          t.q_end = std::min<int32_t>(k.t.q_end, k.t.q_begin + (int32_t)(t1 * qt));
+          t.q_full = std::min(std::max(k.t.q_full, t.q_begin), t.q_end);
+          t.slot = slot0 + (int32_t)q;
+          split.push_back(KeyedB{(int64_t)(t.q_end - t.q_begin), t});
+        }
+      }
+      bt.swap(split);
     }
     std::stable_sort(bt.begin(), bt.end(), [](const KeyedB& a, const KeyedB& b) { return a.work > b.work; });
     for (auto& k : bt) P.bwd_tiles.push_back(k.t);
@@ -284,6 +320,7 @@ void pack_image(Plan& P) {
   P.off_groups = append(P.image, P.groups);
   P.off_fwd = append(P.image, P.fwd_tiles);
   P.off_bwd = append(P.image, P.bwd_tiles);
+  P.off_splits = append(P.image, P.kv_splits);
   if (P.rope_theta > 0.f) {
     P.off_pos_block = append(P.image, P.pos_block);
     P.off_pos_qmain = append(P.image, P.pos_qmain);
