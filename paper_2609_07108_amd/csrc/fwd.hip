@@ -59,6 +59,12 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
 
   const FwdTile tile = p.tiles[blockIdx.x];
   const SeqInfo seq = p.seqs[tile.seq];
+  if (MODE == kModeStep && !p.acc_first) {
+    // a later ring step whose block this tile cannot see leaves the running
+    // sums as they are: nothing to load or write
+    const int j = ((p.rank - p.step_first) % p.C + p.C) % p.C;
+    if (visible_keys(p.toks[tile.tok_begin + tile.ntok - 1].P, j, p.C, seq.c) == 0) return;
+  }
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform
