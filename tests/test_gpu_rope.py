@@ -4,9 +4,11 @@ branch member i at anchor + 1 + i) against the fp64 oracle `oracle.rope`,
 which rounds the rotated queries and keys to bfloat16 as the library hands
 them to its bfloat16 kernels.  Same tolerances as the plain path.  Cases:
 both branch kinds, both ring schedules, both gradient dtypes, both
-branch-array layouts, GQA ratios 4 and 8, and positions up to 8191 with
-theta 1e4 (angles of thousands of radians, so the turn reduction of the
-angles matters).
+branch-array layouts, GQA ratios 1, 4, 8 and 64, an empty sequence, DFlash
+blocks in a sequence that also trains its main tokens, a DFlash-only share,
+EAGLE chains of the maximum 64 members, and positions up to 8191 with theta
+1e4 (angles of thousands of radians, so the turn reduction of the angles
+matters).
 """
 
 import numpy as np
@@ -31,6 +33,14 @@ def case(name):
                         seed=301, name=name)
     if name == "long_cp4":
         return W.custom([8192], [("eagle", 2)], hq=8, hkv=1, cp_size=4, cp_rank=1, seed=302, name=name)
+    if name == "edges_g1":
+        # G = 1, an empty sequence, DFlash blocks of 8 (two per window) in a
+        # sequence that also trains its main tokens, an EAGLE chain of 64
+        return W.custom([0, 512, 64], [None, ("dflash", 8, 32, 2), ("eagle", 64)], hq=2, hkv=2, cp_size=2,
+                        cp_rank=0, seed=303, has_main=[True, True, True], name=name)
+    if name == "dflash_only_g64":
+        # G = 64 and a share whose only queries are DFlash blocks
+        return W.custom([1024], [("dflash", 16, 64)], hq=64, hkv=1, cp_size=2, cp_rank=1, seed=304, name=name)
     raise KeyError(name)
 
 
@@ -55,6 +65,8 @@ def oracle_rope_run(prob, t, theta):
     ("mixed_cp2", "fused", "depth", torch.float32, 5.0e5),
     ("long_cp4", "per_step", "depth", torch.float32, 1.0e4),
     ("long_cp4", "fused", "group", torch.bfloat16, 1.0e4),
+    ("edges_g1", "per_step", "depth", torch.bfloat16, 1.0e4),
+    ("dflash_only_g64", "fused", "group", torch.float32, 1.0e6),
 ])
 def test_rope_forward_backward_parity(cuda, name, mode, layout, grad_dtype, theta):
     prob = case(name)
