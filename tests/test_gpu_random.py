@@ -1,0 +1,88 @@
+"""Seeded random problems: GPU parity against the fp64 oracle on shapes no
+hand-picked case covers.  Each seed draws a context-parallel size and rank,
+1-3 packed sequences of random lengths (multiples of 2C up to 512 tokens,
+some empty), per sequence no branches / an EAGLE-3 chain of random depth / DFlash blocks of a
+random size (one or two per window, with or without main queries), a GQA
+ratio, the branch-array layout, the ring schedule, the gradient dtype and
+rotary embedding on or off.  Same tolerances as the hand-picked cases.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import rope
+from paper_2609_07108_amd import binding as B
+from paper_2609_07108_amd import rankshare as RS
+from paper_2609_07108_amd import workloads as W
+from tests import gpu_helpers as H
+
+pytestmark = pytest.mark.gpu
+
+HEADS = [(2, 1), (4, 2), (8, 2), (6, 3), (16, 4), (12, 4), (32, 8), (8, 8), (10, 5), (64, 2)]
+
+
+def draw_case(seed):
+    rng = np.random.default_rng(1000 + seed)
+    C = int(rng.choice([1, 2, 3, 4, 8]))
+    r = int(rng.integers(C))
+    ns = int(rng.integers(1, 4))
+    lens, spec, has_main = [], [], []
+    for _ in range(ns):
+        L = 2 * C * int(rng.integers(0, max(2, 512 // (2 * C))))
+        kind = rng.choice(["none", "eagle", "dflash"], p=[0.2, 0.45, 0.35])
+        if kind == "eagle" and L:
+            spec.append(("eagle", int(rng.integers(1, 9))))
+            has_main.append(True)
+        elif kind == "dflash" and L >= 16:
+            bs = int(rng.choice([4, 8, 16, 32]))
+            nb = int(rng.integers(1, 3))
+            window = bs * int(rng.integers(2, 5))
+            window = min(window, L)
+            spec.append(("dflash", bs, window, nb))
+            has_main.append(bool(rng.integers(2)))
+        else:
+            spec.append(None)
+            has_main.append(True)
+        lens.append(L)
+    hq, hkv = HEADS[int(rng.integers(len(HEADS)))]
+    prob = W.custom(lens, spec, hq=hq, hkv=hkv, cp_size=C, cp_rank=r, seed=2000 + seed, has_main=has_main,
+                    anchor_seed=3000 + seed, name=f"random{seed}")
+    opts = dict(layout=str(rng.choice(["group", "depth"])),
+                mode=str(rng.choice(["per_step", "fused"])),
+                grad=torch.float32 if rng.integers(2) else torch.bfloat16,
+                theta=float(rng.choice([0.0, 1.0e4, 5.0e5])))
+    return prob, opts
+
+
+@pytest.fixture(scope="module")
+def cuda():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+    return torch.device("cuda:0")
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_problem_parity(cuda, seed):
+    prob, o = draw_case(seed)
+    print(f"[random {seed}] lens {list(np.diff(prob.cu_seqlens))} C={prob.cp_size} r={prob.cp_rank} "
+          f"heads {prob.hq}/{prob.hkv} groups {len(prob.g_len)} {o}", flush=True)
+    mq, bq = oracle.select_queries(prob)
+    if len(mq) + len(bq) == 0:
+        pytest.skip("the drawn share has no queries")
+    t = H.oracle_inputs(prob)
+    args = [t[k] for k in H.TENSORS]
+    dom, dob = t["dom"][mq], t["dob"][bq]
+    if o["theta"]:
+        ref_f = rope.forward(prob, *args, o["theta"], rounded=True, main_q=mq, br_q=bq)
+        ref_b = rope.backward(prob, *args, dom, dob, o["theta"], main_q=mq, br_q=bq, rounded=True)
+    else:
+        ref_f = oracle.forward(prob, *args, mq, bq)
+        ref_b = oracle.backward(prob, *args, dom, dob, mq, bq)
+    share = RS.build_share(prob, device="cuda", layout=o["layout"], rope_theta=o["theta"])
+    mode = B.BA_MODE_FUSED if o["mode"] == "fused" else B.BA_MODE_PER_STEP
+    got_f, got_b, _ = H.gpu_bwd(share, mode, mq, bq, grad_dtype=o["grad"])
+    H.assert_fwd_close(got_f, ref_f)
+    H.assert_bwd_close(got_b, ref_b)
