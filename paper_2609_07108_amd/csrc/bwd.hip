@@ -1069,24 +1069,31 @@ __global__ __launch_bounds__(256) void bwd_dq_finalize_kernel(BwdParams p) {
     }
     const int64_t kvcol = (int64_t)(h / p.G) * kHeadDim + c8;
     const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
-    for (int b = 0; __ballot(b < nb) != 0; ++b) {
-      const bool active = b < nb;
-      // inactive rows read their group's first key (main rows: branch row 0)
-      const int64_t krow = (int64_t)gi.row0 + (int64_t)(active ? b : 0) * gi.stride;
-      const bf16x8 kv = ld16(p.k_br + krow * kv_row_stride + kvcol);
-      const bf16x8 vv = ld16(p.v_br + krow * kv_row_stride + kvcol);
-      float sd = 0.f, pd = 0.f;
+    // keys in groups of four, all four loaded before any is used
+    for (int b0 = 0; __ballot(b0 < nb) != 0; b0 += 4) {
+      bf16x8 kv[4], vv[4];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        sd = fmaf(qf[e], (float)kv[e], sd);
-        pd = fmaf(gf[e], (float)vv[e], pd);
+      for (int u = 0; u < 4; ++u) {
+        // keys past the row's last read its group's first key (main rows: branch row 0)
+        const int64_t krow = (int64_t)gi.row0 + (int64_t)(b0 + u < nb ? b0 + u : 0) * gi.stride;
+        kv[u] = ld16(p.k_br + krow * kv_row_stride + kvcol);
+        vv[u] = ld16(p.v_br + krow * kv_row_stride + kvcol);
       }
-      sd = row16_sum(sd);
-      pd = row16_sum(pd);
-      const float pr = active ? fast_exp2(fmaf(sd, p.scale_log2, rs.x)) : 0.f;
-      const float ds = pr * (pd + rs.y);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = fmaf(ds, (float)kv[e], acc[e]);
+      for (int u = 0; u < 4; ++u) {
+        float sd = 0.f, pd = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          sd = fmaf(qf[e], (float)kv[u][e], sd);
+          pd = fmaf(gf[e], (float)vv[u][e], pd);
+        }
+        sd = row16_sum(sd);
+        pd = row16_sum(pd);
+        const float pr = b0 + u < nb ? fast_exp2(fmaf(sd, p.scale_log2, rs.x)) : 0.f;
+        const float ds = pr * (pd + rs.y);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf(ds, (float)kv[u][e], acc[e]);
+      }
     }
   }
   if (!live) return;

@@ -534,25 +534,38 @@ __global__ __launch_bounds__(256) void fwd_finalize_kernel(FwdParams p) {
     for (int e = 0; e < 8; ++e) qf[e] = (float)qv[e];
     const int64_t kvcol = (int64_t)(h / p.G) * kHeadDim + c8;
     const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
-    for (int b = 0; __ballot(b < nb) != 0; ++b) {
-      const bool active = b < nb;
-      // inactive rows read their group's first key (main rows: branch row 0)
-      const int64_t krow = (int64_t)gi.row0 + (int64_t)(active ? b : 0) * gi.stride;
-      const bf16x8 kv = ld16(p.k_br + krow * kv_row_stride + kvcol);
-      const bf16x8 vv = ld16(p.v_br + krow * kv_row_stride + kvcol);
-      float dot = 0.f;
+    // keys in groups of four, all four loaded before any is used
+    for (int b0 = 0; __ballot(b0 < nb) != 0; b0 += 4) {
+      bf16x8 kv[4], vv[4];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) dot = fmaf(qf[e], (float)kv[e], dot);
-      dot = row16_sum(dot);
-      if (active) {
-        const float x = dot * p.scale_log2;
-        const float m_new = fmaxf(mb, x);
-        const float alpha = fast_exp2(mb - m_new);
-        const float ex = fast_exp2(x - m_new);
-        lb = lb * alpha + ex;
+      for (int u = 0; u < 4; ++u) {
+        // keys past the row's last read its group's first key (main rows: branch row 0)
+        const int64_t krow = (int64_t)gi.row0 + (int64_t)(b0 + u < nb ? b0 + u : 0) * gi.stride;
+        kv[u] = ld16(p.k_br + krow * kv_row_stride + kvcol);
+        vv[u] = ld16(p.v_br + krow * kv_row_stride + kvcol);
+      }
+      float x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        float dot = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dot = fmaf(qf[e], (float)kv[u][e], dot);
+        dot = row16_sum(dot);  // every lane takes part in the row sum
+        x[u] = b0 + u < nb ? dot * p.scale_log2 : -INFINITY;
+      }
+      if (b0 < nb) {
+        const float m_new = fmaxf(fmaxf(mb, fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
+        const float alpha = fast_exp2(mb - m_new);  // mb = -inf at the first key: 0
+        float ex[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) ex[u] = fast_exp2(x[u] - m_new);  // keys past the last: 0
+        lb = lb * alpha + ((ex[0] + ex[1]) + (ex[2] + ex[3]));
         mb = m_new;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) ob[e] = fmaf(ob[e], alpha, ex * (float)vv[e]);
+        for (int e = 0; e < 8; ++e)
+          ob[e] = fmaf(ob[e], alpha,
+                       fmaf(ex[0], (float)vv[0][e],
+                            fmaf(ex[1], (float)vv[1][e], fmaf(ex[2], (float)vv[2][e], ex[3] * (float)vv[3][e]))));
       }
     }
   }
