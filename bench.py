@@ -140,7 +140,8 @@ def main():
     ap.add_argument("--config", type=int, default=4, help="named workload 1..5 (4 = 256K headline)")
     ap.add_argument("--mode", choices=["fused", "per_step"], default="per_step",
                     help="per_step: one launch per ring step (the ring's schedule); fused: one walk over all blocks")
-    ap.add_argument("--cpu-rows", type=int, default=24, help="oracle sample size (0 disables)")
+    ap.add_argument("--cpu-rows", type=int, default=48,
+                    help="query rows of the CPU oracle sample (about 12 s on 16 cores; 0 disables)")
     ap.add_argument("--rope", type=float, default=0.0, metavar="THETA",
                     help="rotate queries and keys by their positions (rotary embedding, base THETA) "
                          "in front of the attention; 0 (default) leaves them as they are")
