@@ -127,9 +127,15 @@ def cpu_baseline(prob, rows: int, seed: int = 1234):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         cores = os.cpu_count()
+    cpu = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": (f_fwd + f_bwd) / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{len(sm)} main + {len(sb)} branch query rows of the share, fp64 fwd+bwd against "
-                      f"all their keys, {dt:.1f} s", "seconds": round(dt, 2)}
+                      f"all their keys, {dt:.1f} s", "seconds": round(dt, 2), "cpu": cpu}
 
 
 def main():
