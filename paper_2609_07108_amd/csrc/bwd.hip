@@ -956,18 +956,30 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
     if (MODE == kModeStep) {
       if (!valid[rb]) return;
       float* dst = p.dq_acc + acc_row * kHeadDim;
+      // the running sums of the row, every load issued before any is used
+      float4 prev[4][4];
+      if (!p.acc_first) {
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int vq = 0; vq < 4; ++vq)
+            prev[dt][vq] = *reinterpret_cast<const float4*>(dst + 32 * dt + 8 * vq + 4 * half);
+      } else {
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int vq = 0; vq < 4; ++vq) prev[dt][vq] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
         for (int vq = 0; vq < 4; ++vq) {
-          float4* d4 = reinterpret_cast<float4*>(dst + 32 * dt + 8 * vq + 4 * half);
-          float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (!p.acc_first) a = *d4;
+          float4 a = prev[dt][vq];
           a.x += st[dt][4 * vq + 0];
           a.y += st[dt][4 * vq + 1];
           a.z += st[dt][4 * vq + 2];
           a.w += st[dt][4 * vq + 3];
-          *d4 = a;
+          *reinterpret_cast<float4*>(dst + 32 * dt + 8 * vq + 4 * half) = a;
         }
       return;
     }

@@ -365,8 +365,16 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
         const float inv = 1.f / l_tot[rb];
         float wa = 0.f, wb = inv;
         float lse_new = lse2;
+        // the running pair of the row, every load issued before any is used
+        float4 prev[4][4];
+        float la = -INFINITY;
         if (!p.acc_first) {
-          const float la = p.lse_acc[acc_row];
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+            for (int vq = 0; vq < 4; ++vq)
+              prev[dt][vq] = *reinterpret_cast<const float4*>(oacc + 32 * dt + 8 * vq + 4 * half);
+          la = p.lse_acc[acc_row];
           const float hi = fmaxf(la, lse2);
           const float ea = fast_exp2(la - hi);  // la = -inf gives 0
           const float eb = fast_exp2(lse2 - hi);
@@ -374,20 +382,23 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
           lse_new = hi + __log2f(tot);
           wa = ea / tot;
           wb = eb / tot * inv;
+        } else {
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+            for (int vq = 0; vq < 4; ++vq) prev[dt][vq] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
           for (int vq = 0; vq < 4; ++vq) {
-            float4* dst = reinterpret_cast<float4*>(oacc + 32 * dt + 8 * vq + 4 * half);
-            float4 prev = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (!p.acc_first) prev = *dst;
+            const float4 pr = prev[dt][vq];
             float4 r;
-            r.x = wa * prev.x + wb * st_o[dt][4 * vq + 0];
-            r.y = wa * prev.y + wb * st_o[dt][4 * vq + 1];
-            r.z = wa * prev.z + wb * st_o[dt][4 * vq + 2];
-            r.w = wa * prev.w + wb * st_o[dt][4 * vq + 3];
-            *dst = r;
+            r.x = wa * pr.x + wb * st_o[dt][4 * vq + 0];
+            r.y = wa * pr.y + wb * st_o[dt][4 * vq + 1];
+            r.z = wa * pr.z + wb * st_o[dt][4 * vq + 2];
+            r.w = wa * pr.w + wb * st_o[dt][4 * vq + 3];
+            *reinterpret_cast<float4*>(oacc + 32 * dt + 8 * vq + 4 * half) = r;
           }
         }
         if (half == 0) p.lse_acc[acc_row] = lse_new;
