@@ -697,23 +697,23 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
   bool valid[2];
   TokInfo tk[2];
   float nl2[2], ndl[2];  // -LSE log2 e, -Delta
+  // (the token records and row statistics of both row blocks are read
+  // before any Q or dO load is issued: a compiler-visible load after the
+  // untracked loads would wait for them too)
   bf16x8 qreg[2][8], greg[2][8];
+  const bf16* qp[2];
+  const bf16* gp[2];
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb) {
     const int row = 64 * wave + 32 * rb + qi;
     const int tl = row / p.G;
     head[rb] = tile.kvh * p.G + (row - tl * p.G);
     valid[rb] = tl < tile.ntok;
-    tk[rb] = valid[rb] ? p.toks[tile.tok_begin + tl] : TokInfo{0, -1, -1, -1};
-    const TokInfo tq = valid[rb] ? tk[rb] : p.toks[tile.tok_begin + tile.ntok - 1];
+    const TokInfo tq = p.toks[tile.tok_begin + (valid[rb] ? tl : tile.ntok - 1)];  // one unconditional load
+    tk[rb] = valid[rb] ? tq : TokInfo{0, -1, -1, -1};
     const int hq_row = valid[rb] ? head[rb] : tile.kvh * p.G;
-    const bf16* qp = row_ptr(p.q_main, p.q_br, tq.qrow, p.hq, hq_row);
-    const bf16* gp = row_ptr(p.do_main, p.do_br, tq.qrow, p.hq, hq_row);
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      load16_agpr(qreg[rb][c], qp + 16 * c + 8 * half);
-      load16_agpr(greg[rb][c], gp + 16 * c + 8 * half);
-    }
+    qp[rb] = row_ptr(p.q_main, p.q_br, tq.qrow, p.hq, hq_row);
+    gp[rb] = row_ptr(p.do_main, p.do_br, tq.qrow, p.hq, hq_row);
     nl2[rb] = -INFINITY;
     ndl[rb] = 0.f;
     if (valid[rb]) {
@@ -722,6 +722,13 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
       ndl[rb] = rs.y;
     }
   }
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      load16_agpr(qreg[rb][c], qp[rb] + 16 * c + 8 * half);
+      load16_agpr(greg[rb][c], gp[rb] + 16 * c + 8 * half);
+    }
   __builtin_amdgcn_s_waitcnt(0);
 
   f32x16 dq[2][4];

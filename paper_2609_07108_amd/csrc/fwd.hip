@@ -79,21 +79,27 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
   // B operand of S^T = K Q^T (Q^T: k = head dims, n = rows), resident in the
   // accumulation registers; rows without a token load a row of the tile's
   // last token (finite, and their results are never written)
+  // (the token records of both row blocks are read before any Q load is
+  // issued: a compiler-visible load after the untracked Q loads would wait
+  // for them too)
   bf16x8 qreg[2][8];
+  const bf16* qptr[2];
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb) {
     const int row = 64 * wave + 32 * rb + qi;
     const int tl = row / p.G;
     head[rb] = tile.kvh * p.G + (row - tl * p.G);
     valid[rb] = tl < tile.ntok;
-    tk[rb] = valid[rb] ? p.toks[tile.tok_begin + tl] : TokInfo{0, -1, -1, -1};
-    const TokInfo tq = valid[rb] ? tk[rb] : p.toks[tile.tok_begin + tile.ntok - 1];
+    const TokInfo tq = p.toks[tile.tok_begin + (valid[rb] ? tl : tile.ntok - 1)];  // one unconditional load
+    tk[rb] = valid[rb] ? tq : TokInfo{0, -1, -1, -1};
     const int hq_row = valid[rb] ? head[rb] : tile.kvh * p.G;
-    const bf16* qptr = tq.qrow >= 0 ? p.q_main + ((int64_t)tq.qrow * p.hq + hq_row) * kHeadDim
-                                    : p.q_br + ((int64_t)(-tq.qrow - 1) * p.hq + hq_row) * kHeadDim;
-#pragma unroll
-    for (int c = 0; c < 8; ++c) load16_agpr(qreg[rb][c], qptr + 16 * c + 8 * half);
+    qptr[rb] = tq.qrow >= 0 ? p.q_main + ((int64_t)tq.qrow * p.hq + hq_row) * kHeadDim
+                            : p.q_br + ((int64_t)(-tq.qrow - 1) * p.hq + hq_row) * kHeadDim;
   }
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) load16_agpr(qreg[rb][c], qptr[rb] + 16 * c + 8 * half);
   __builtin_amdgcn_s_waitcnt(0);
 
   f32x16 o[2][4];  // O^T accumulators, d = 32 dt + 8 (v/4) + 4 half + v%4
