@@ -63,6 +63,26 @@ struct RopeFreq {
   float hi, lo;
 };
 
+// The 64 frequencies of base theta (> 0), computed in double and split.
+void rope_freq_table(float theta, RopeFreq* out);
+
+// sin and cos of the angle of dim pair f at position pos.  The turns
+// pos * f are formed as an unevaluated float sum, the product's rounding
+// error recovered with an fma, and the whole turns are removed before the
+// sum is rounded, so the angle stays within ~1e-7 rad of the exact one at
+// every position below 2^24.  Contraction stays off: fusing p * hi into
+// the subtraction of the whole turns would count the product's rounding
+// error twice (once there, once in tl), an angle error of up to half an ulp
+// of the turn count.
+__device__ __forceinline__ void rope_sincos(int pos, RopeFreq f, float& s, float& c) {
+#pragma clang fp contract(off)
+  const float p = (float)pos;
+  const float th = p * f.hi;
+  const float tl = fmaf(p, f.lo, fmaf(p, f.hi, -th));
+  const float r = (th - rintf(th)) + tl;  // fraction of a turn in [-0.5, 0.5]
+  sincospif(2.f * r, &s, &c);
+}
+
 struct FwdTile {
   int32_t seq;
   int32_t tok_begin;

@@ -21,19 +21,6 @@ namespace {
 
 constexpr int kRopeHeads = 4;  // heads loaded together, before any is used
 
-// sin and cos of the angle of dim pair f at position pos.  The turns
-// pos * f (f = theta^(-j/64) / 2 pi as hi + lo) are formed as an unevaluated
-// float sum, the product's rounding error recovered with an fma, and the
-// whole turns are removed before the sum is rounded, so the angle stays
-// within ~1e-7 rad of the exact one at every position below 2^24.
-__device__ __forceinline__ void rope_sincos(int pos, RopeFreq f, float& s, float& c) {
-  const float p = (float)pos;
-  const float th = p * f.hi;
-  const float tl = fmaf(p, f.lo, fmaf(p, f.hi, -th));
-  const float r = (th - rintf(th)) + tl;  // fraction of a turn in [-0.5, 0.5]
-  sincospif(2.f * r, &s, &c);
-}
-
 __device__ __forceinline__ void load8(const bf16* p, float (&x)[8]) {
   const bf16x8 v = ld16(p);
 #pragma unroll
