@@ -215,6 +215,14 @@ void branch_attn_plan_destroy(ba_plan* plan);
  * or non-finite theta, BA_E_UNSUPPORTED if a position reaches 2^24. */
 int branch_attn_plan_set_rope(ba_plan* plan, float theta);
 
+/* Positions of the plan's rows, host arrays filled by the call:
+ * main_pos[u] (n_local entries) is the position in its sequence of local
+ * main row u, br_pos[b] (num_branch_rows entries) is a + 1 + i for member i
+ * of a group anchored at a, -1 for a row of no group.  The positions the
+ * rotary embedding of branch_attn_plan_set_rope uses, and the ones to pass to
+ * branch_attn_qkv_fwd / _bwd.  Either pointer may be NULL (skipped). */
+int branch_attn_plan_positions(const ba_plan* plan, int32_t* main_pos, int32_t* br_pos);
+
 /* Workspace bytes needed by branch_attn_fwd / branch_attn_bwd in `mode`. */
 int branch_attn_workspace_size(const ba_plan* plan, int32_t mode, size_t* fwd_bytes,
                                size_t* bwd_bytes);
@@ -266,6 +274,52 @@ int branch_attn_bwd(void* stream, const ba_plan* plan, int32_t mode, const ba_bw
  * `stream`; rows == 0 is a no-op. */
 int lse_merge(void* stream, int64_t rows, int32_t heads, int32_t head_dim, float* o_acc,
               float* lse_acc, const void* o_part, int32_t o_part_dtype, const float* lse_part);
+
+/* ------------------------------------------- QKV projection (draft layer)
+ *
+ * The step in front of the op inside a draft layer (Sec. 3.2 builds the
+ * draft's attention on the target's decoder layer): grouped-query projection
+ * of hidden states to q-, k- and v-heads, with the rotary embedding of
+ * branch_attn_plan_set_rope applied to the queries and keys.  Plan-free: the
+ * caller projects the main rows and the branch rows in separate calls, with
+ * the positions of branch_attn_plan_positions, and hands the results to
+ * branch_attn_fwd with the plan's own rotation off (theta 0).
+ *
+ *   x    bf16 [rows, hidden], hidden a positive multiple of 128
+ *   w    bf16 [(hq + 2 hkv) * 128, hidden]: the fused q/k/v weight of a
+ *        linear layer (output-major, like torch.nn.Linear.weight), rows
+ *        0 .. hq*128-1 the q-heads, then hkv k-heads, then hkv v-heads
+ *   pos  int32 [rows], device; a row with a negative position is not
+ *        rotated; read only when theta > 0 (positions below 2^24 keep the
+ *        angle error near 1e-7 rad)
+ *   theta  rotary base (> 0), or 0 for no rotation
+ * All device pointers 16-byte aligned; hq % hkv == 0.  BA_E_INVAL for
+ * malformed arguments, BA_E_UNSUPPORTED for a hidden size that is not a
+ * multiple of 128.  rows == 0 is a no-op (the backward still clears dw
+ * unless accumulate_dw).  Asynchronous on `stream`. */
+
+/* q = R(pos) (x W_q^T), k = R(pos) (x W_k^T), v = x W_v^T, fp32 accumulation,
+ * each rounded once to bf16 (RNE): q [rows, hq, 128], k and v
+ * [rows, hkv, 128]. */
+int branch_attn_qkv_fwd(void* stream, int64_t rows, int32_t hidden, int32_t hq, int32_t hkv, const void* x,
+                        const void* w, const int32_t* pos, float theta, void* q, void* k, void* v);
+
+/* Backward of branch_attn_qkv_fwd for the loss gradients dq, dk, dv (dtype
+ * grad_dtype, the layouts of q, k, v; the gradients of the rotated queries
+ * and keys, as branch_attn_bwd returns them for a plan without rotation):
+ * dY = [R^T dq, R^T dk, dv] rounded to bf16 into the workspace, then
+ *   dx [rows, hidden] (dtype dx_dtype) = dY W,
+ *   dw [(hq + 2 hkv) * 128, hidden] fp32 = dY^T x, or dw += dY^T x when
+ *   accumulate_dw is non-zero (main and branch rows share the weight).
+ * The workspace (device, 256-byte aligned) holds at least the bytes of
+ * branch_attn_qkv_workspace_size; BA_E_WORKSPACE otherwise. */
+int branch_attn_qkv_bwd(void* stream, int64_t rows, int32_t hidden, int32_t hq, int32_t hkv, const void* x,
+                        const void* w, const int32_t* pos, float theta, const void* dq, const void* dk,
+                        const void* dv, int32_t grad_dtype, void* dx, int32_t dx_dtype, float* dw,
+                        int32_t accumulate_dw, void* workspace, size_t workspace_bytes);
+
+/* Workspace bytes of branch_attn_qkv_bwd: rows * (hq + 2 hkv) * 128 * 2. */
+int branch_attn_qkv_workspace_size(int64_t rows, int32_t hq, int32_t hkv, size_t* bytes);
 
 #ifdef __cplusplus
 }

@@ -20,7 +20,9 @@ the chain rule through the merge, central finite differences, reassembly of
 all context-parallel ranks, and the closed-form zigzag pair counts.
 :mod:`oracle.rope` adds rotary position embedding in front of the op
 (pinned against the Llama rotary routine of the transformers library, the
-relative-position identity and finite differences).
+relative-position identity and finite differences); :mod:`oracle.qkv` the
+grouped-query QKV projection with that rotation (pinned against torch's
+linear layer plus the same library routine, and finite differences).
 """
 
 from .attention import (  # noqa: F401
@@ -28,3 +30,4 @@ from .attention import (  # noqa: F401
     lse_merge, lse_merge_backward, allowed_pair_counts, useful_flops,
 )
 from . import rope  # noqa: F401
+from . import qkv  # noqa: F401

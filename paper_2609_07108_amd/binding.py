@@ -33,7 +33,8 @@ BA_MODE_FUSED = 1
 EXPORTED = ("zigzag_partition", "branch_attn_plan_create", "branch_attn_plan_destroy",
             "branch_attn_workspace_size", "branch_attn_plan_info", "branch_attn_useful_flops",
             "branch_attn_pair_counts", "branch_attn_last_error", "branch_attn_fwd", "branch_attn_bwd",
-            "lse_merge", "branch_attn_plan_set_rope")
+            "lse_merge", "branch_attn_plan_set_rope", "branch_attn_plan_positions", "branch_attn_qkv_fwd",
+            "branch_attn_qkv_bwd", "branch_attn_qkv_workspace_size")
 
 c_i32 = ctypes.c_int32
 c_vp = ctypes.c_void_p
@@ -101,6 +102,13 @@ def lib() -> ctypes.CDLL:
         L.branch_attn_fwd.argtypes = [c_vp, c_vp, c_i32, ctypes.POINTER(BaFwdIO), c_vp, ctypes.c_size_t]
         L.branch_attn_bwd.argtypes = [c_vp, c_vp, c_i32, ctypes.POINTER(BaBwdIO), c_vp, ctypes.c_size_t]
         L.lse_merge.argtypes = [c_vp, ctypes.c_int64, c_i32, c_i32, c_vp, c_vp, c_vp, c_i32, c_vp]
+        L.branch_attn_plan_positions.argtypes = [c_vp, ctypes.POINTER(c_i32), ctypes.POINTER(c_i32)]
+        L.branch_attn_qkv_fwd.argtypes = [c_vp, ctypes.c_int64, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp,
+                                          ctypes.c_float, c_vp, c_vp, c_vp]
+        L.branch_attn_qkv_bwd.argtypes = [c_vp, ctypes.c_int64, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp,
+                                          ctypes.c_float, c_vp, c_vp, c_vp, c_i32, c_vp, c_i32, c_vp, c_i32,
+                                          c_vp, ctypes.c_size_t]
+        L.branch_attn_qkv_workspace_size.argtypes = [ctypes.c_int64, c_i32, c_i32, ctypes.POINTER(ctypes.c_size_t)]
         _lib = L
     return _lib
 
@@ -174,6 +182,14 @@ class Plan:
         """Rotary position embedding in front of the attention (theta 0: off)."""
         _check(lib().branch_attn_plan_set_rope(self._h, float(theta)))
 
+    def positions(self, n_local: int, num_branch_rows: int):
+        """(main_pos [n_local], br_pos [num_branch_rows]) int32 host arrays."""
+        mp = np.zeros(max(n_local, 1), np.int32)
+        bp = np.zeros(max(num_branch_rows, 1), np.int32)
+        P = ctypes.POINTER(c_i32)
+        _check(lib().branch_attn_plan_positions(self._h, mp.ctypes.data_as(P), bp.ctypes.data_as(P)))
+        return mp[:n_local], bp[:num_branch_rows]
+
     def workspace_size(self, mode: int):
         f, b = ctypes.c_size_t(), ctypes.c_size_t()
         _check(lib().branch_attn_workspace_size(self._h, int(mode), ctypes.byref(f), ctypes.byref(b)))
@@ -226,3 +242,33 @@ def lse_merge(o_acc, lse_acc, o_part, lse_part, stream=None):
     dt = BA_DTYPE_BF16 if o_part.dtype == torch.bfloat16 else BA_DTYPE_F32
     _check(lib().lse_merge(_stream(stream), rows, heads, d, _ptr(o_acc), _ptr(lse_acc), _ptr(o_part), dt,
                            _ptr(lse_part)))
+
+
+# ------------------------------------------------------- QKV projection
+
+def branch_attn_qkv_workspace_size(rows: int, hq: int, hkv: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().branch_attn_qkv_workspace_size(int(rows), int(hq), int(hkv), ctypes.byref(n)))
+    return n.value
+
+
+def branch_attn_qkv_fwd(x, w, hq: int, hkv: int, pos, theta: float, q, k, v, stream=None):
+    """x [rows, hidden] bf16, w [(hq + 2 hkv) * 128, hidden] bf16, pos [rows] int32 (or None when
+    theta == 0); writes q [rows, hq, 128], k and v [rows, hkv, 128] (bf16)."""
+    rows, hidden = x.shape
+    _check(lib().branch_attn_qkv_fwd(_stream(stream), int(rows), int(hidden), int(hq), int(hkv), _ptr(x), _ptr(w),
+                                     _ptr(pos), float(theta), _ptr(q), _ptr(k), _ptr(v)))
+
+
+def branch_attn_qkv_bwd(x, w, hq: int, hkv: int, pos, theta: float, dq, dk, dv, dx, dw,
+                        accumulate_dw: bool, workspace, stream=None):
+    """Gradients dx (dtype of the dx tensor) and dw (fp32, overwritten or accumulated) of the
+    projection for dq / dk / dv of one dtype (bf16 or fp32)."""
+    import torch
+    rows, hidden = x.shape
+    gd = BA_DTYPE_F32 if dq.dtype == torch.float32 else BA_DTYPE_BF16
+    xd = BA_DTYPE_F32 if dx.dtype == torch.float32 else BA_DTYPE_BF16
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().branch_attn_qkv_bwd(_stream(stream), int(rows), int(hidden), int(hq), int(hkv), _ptr(x), _ptr(w),
+                                     _ptr(pos), float(theta), _ptr(dq), _ptr(dk), _ptr(dv), gd, _ptr(dx), xd,
+                                     _ptr(dw), 1 if accumulate_dw else 0, _ptr(workspace), ws_bytes))

@@ -20,7 +20,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_lib")
 LIB_NAME = "libbranchattn.so"
 
-HIP_SOURCES = ["plan.hip", "lse_merge.hip", "fwd.hip", "bwd.hip", "rope.hip", "api.hip"]
+HIP_SOURCES = ["plan.hip", "lse_merge.hip", "fwd.hip", "bwd.hip", "rope.hip", "proj.hip", "api.hip"]
 HOST_SOURCES = []
 
 ARCH = "gfx950"

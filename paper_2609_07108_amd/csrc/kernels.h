@@ -105,4 +105,41 @@ hipError_t launch_rope_rows(const bf16* src, bf16* dst, const int32_t* pos, cons
 hipError_t launch_rope_grad(const float* src, void* dst, bool dst_f32, const int32_t* pos, const RopeFreq* freq,
                             int64_t rows, int heads, bool rotate, hipStream_t stream);
 
+
+// Grouped-query QKV projection (proj.hip): C[i][j] = sum_k A(i,k) B(j,k) over
+// 128 x 128 tiles.  An operand is stored k-major ([i][k], ld elements per
+// row; its reduction slices must lie inside K) or i-major ([k][i]; its row
+// count must be a multiple of 128, a ragged K is allowed).  J is a multiple
+// of 128; I may be ragged where A is k-major.
+constexpr int kProjEpiPlain = 0;  // C written row-major (ldc), bf16 or fp32, optionally added to
+constexpr int kProjEpiQkv = 1;    // 128-column heads split into q / k / v, q and k rotated, bf16 THD
+
+struct RopeFreqTable {
+  RopeFreq f[kHeadDim / 2];
+};
+
+struct ProjGemmParams {
+  const bf16* a;
+  const bf16* b;
+  int64_t lda, ldb;
+  int64_t I, K;
+  int32_t J;
+  // plain epilogue
+  int32_t c_f32, accumulate;
+  void* c;
+  int64_t ldc;
+  // q / k / v epilogue
+  bf16* q;
+  bf16* k;
+  bf16* v;
+  int32_t hq, hkv, rotate;
+  const int32_t* pos;
+  RopeFreqTable freq;
+};
+
+hipError_t launch_proj_gemm(const ProjGemmParams& p, bool a_imajor, bool b_imajor, int epi, hipStream_t stream);
+hipError_t launch_proj_grad_pack(const void* dq, const void* dk, const void* dv, bool src_f32, bf16* dy,
+                                 const int32_t* pos, int64_t rows, int hq, int hkv, bool rotate,
+                                 const RopeFreqTable& freq, hipStream_t stream);
+
 }  // namespace ba

@@ -334,6 +334,15 @@ void pack_image(Plan& P) {
 // block (rank j's local order: chunk j, then chunk 2C-1-j of each sequence)
 // and of every branch row (anchor + 1 + member index), and the frequency of
 // each of the 64 dim pairs in turns per position.
+void rope_freq_table(float theta, RopeFreq* out) {
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int j = 0; j < kHeadDim / 2; ++j) {
+    const double f = std::pow((double)theta, -(double)j / (kHeadDim / 2)) / two_pi;
+    const float hi = (float)f;
+    out[j] = RopeFreq{hi, (float)(f - (double)hi)};
+  }
+}
+
 static int build_rope(Plan& P, float theta) {
   if (!std::isfinite(theta) || theta < 0.f) return fail(BA_E_INVAL, "rope theta must be finite and >= 0");
   P.rope_theta = theta;
@@ -371,12 +380,8 @@ static int build_rope(Plan& P, float theta) {
       pack_image(P);
       return fail(BA_E_UNSUPPORTED, "rope positions must stay below 2^24");
     }
-    const double two_pi = 6.283185307179586476925286766559;
-    for (int j = 0; j < kHeadDim / 2; ++j) {
-      const double f = std::pow((double)theta, -(double)j / (kHeadDim / 2)) / two_pi;
-      const float hi = (float)f;
-      P.rope_freq.push_back(RopeFreq{hi, (float)(f - (double)hi)});
-    }
+    P.rope_freq.resize(kHeadDim / 2);
+    rope_freq_table(theta, P.rope_freq.data());
   }
   pack_image(P);
   return BA_OK;
@@ -443,6 +448,25 @@ int branch_attn_plan_set_rope(ba_plan* plan, float theta) {
   } catch (const std::exception& e) {
     return ba::fail(BA_E_INVAL, std::string("rope tables: ") + e.what());
   }
+}
+
+int branch_attn_plan_positions(const ba_plan* plan, int32_t* main_pos, int32_t* br_pos) {
+  if (!plan) return ba::fail(BA_E_INVAL, "plan is NULL");
+  const ba::Plan& P = plan->p;
+  if (main_pos) {
+    const int32_t C = P.cp_size, r = P.cp_rank;
+    for (int32_t s = 0; s < P.num_seqs; ++s) {
+      const ba::SeqInfo& si = P.seqs[s];
+      for (int32_t u = 0; u < 2 * si.c; ++u)
+        main_pos[si.seg_off + u] = u < si.c ? r * si.c + u : (2 * C - 1 - r) * si.c + (u - si.c);
+    }
+  }
+  if (br_pos) {
+    for (int32_t i = 0; i < P.num_branch_rows; ++i) br_pos[i] = -1;
+    for (const ba::GroupInfo& g : P.groups)
+      for (int32_t i = 0; i < g.len; ++i) br_pos[(size_t)g.row0 + (size_t)i * g.stride] = g.anchor + 1 + i;
+  }
+  return BA_OK;
 }
 
 int branch_attn_workspace_size(const ba_plan* plan, int32_t mode, size_t* fwd_bytes, size_t* bwd_bytes) {

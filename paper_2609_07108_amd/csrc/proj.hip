@@ -1,0 +1,465 @@
+// Grouped-query QKV projection of a draft layer's attention input, with the
+// rotary embedding of the queries and keys applied in the projection's
+// epilogue, and its backward.  This is the step in front of branch attention
+// inside a draft layer (Sec. 3.2 builds the draft's attention on the target's
+// decoder layer: hidden states are projected to q-heads and fewer kv-heads,
+// queries and keys rotated by their positions, then attended).
+//
+//   forward:  Y = X W^T, X [rows, hidden], W [(hq + 2 hkv) * 128, hidden]
+//             (the fused q/k/v weight of a linear layer, output-major);
+//             Y's 128-column head blocks are the q-heads, then the k-heads,
+//             then the v-heads; q and k rotated by pos[row] (dims j, j + 64
+//             by the angle pos * theta^(-j/64)), all three written as bf16
+//             [rows, heads, 128].
+//   backward: dY = [R^T dQ, R^T dK, dV] (bf16, in the workspace), then
+//             dX = dY W and dW = dY^T X (fp32 accumulation).
+//
+// One GEMM kernel serves all three products.  C[i][j] = sum_k A(i,k) B(j,k)
+// over 128 x 128 output tiles, 64 reduction values per stage, two stages of
+// LDS; each operand is either stored with its reduction index contiguous
+// ([i][k], "k-major") or with its row index contiguous ([k][i], "i-major").
+// A workgroup of four wavefronts computes one tile, each wavefront a 64 x 64
+// quarter as 2 x 2 v_mfma_f32_32x32x16_bf16 accumulators.  Operands move
+// global -> registers -> LDS while the previous stage is multiplied (the
+// loads of stage t+1 are in flight during the MFMAs of stage t).
+#include <cmath>
+#include <string>
+
+#include "ba_internal.h"
+#include "device_common.h"
+#include "kernels.h"
+
+namespace ba {
+namespace {
+
+constexpr int kTile = 128;               // output tile rows and columns
+constexpr int kBk = 64;                  // reduction values per stage
+constexpr int kOpElems = kTile * kBk;    // one operand tile, bf16 elements (16 KB)
+constexpr int kStageLd = kTile + 8;      // fp32 staging row pitch of the epilogue (conflict-free writes)
+constexpr int kSmemBytes = (4 * kOpElems * 2 > kTile * kStageLd * 4) ? 4 * kOpElems * 2 : kTile * kStageLd * 4;
+
+// k-major operand tile: 128 rows x 64 reduction values, 128 B per row; the
+// eight 16-byte chunks of row r are XOR-permuted by (r/2) % 8, so that the
+// 16 lanes of an MFMA operand read (16 consecutive rows, one chunk) and of a
+// tile store (two rows, eight chunks) touch 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int kmaj_off(int r, int chunk) { return r * kBk + ((chunk ^ ((r >> 1) & 7)) << 3); }
+
+// Global -> register fetch of one operand tile, four 16-byte loads per thread.
+// k-major ([i][k], ld elements per stored row): thread t takes chunk t % 8 of
+// rows t/8 + 32q; rows past the end re-read the last row (their results are
+// never stored).  The caller guarantees the reduction slice lies inside K.
+// i-major ([k][i]): thread t takes columns 8 (t % 16) .. +7 of reduction rows
+// t/16 + 16q; rows at or past K read row K-1 and become zeros, so a ragged
+// reduction end contributes nothing.
+template <bool kIMajor>
+__device__ __forceinline__ void fetch_tile(const bf16* __restrict__ base, int64_t ld, int64_t i0, int64_t ni,
+                                           int64_t k0, int64_t nk, int tid, bf16x8 (&g)[4]) {
+  if constexpr (!kIMajor) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      int64_t row = i0 + (tid >> 3) + 32 * q;
+      row = row < ni ? row : ni - 1;
+      g[q] = ld16(base + row * ld + k0 + 8 * (tid & 7));
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t kk = k0 + (tid >> 4) + 16 * q;
+      const bf16x8 v = ld16(base + (kk < nk ? kk : nk - 1) * ld + i0 + 8 * (tid & 15));
+      g[q] = kk < nk ? v : bf16x8{};
+    }
+  }
+}
+
+template <bool kIMajor>
+__device__ __forceinline__ void store_tile(bf16* T, int tid, const bf16x8 (&g)[4]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if constexpr (!kIMajor)
+      st16(T + kmaj_off((tid >> 3) + 32 * q, tid & 7), g[q]);
+    else
+      st16(T + tile_off<kBk>((tid >> 4) + 16 * q, 8 * (tid & 15)), g[q]);
+  }
+}
+
+// MFMA operand for rows r0 .. r0+31 of a tile at reduction step ks (16
+// values): lane l takes row r0 + l%32, values 16 ks + 8 (l/32) .. +7.
+template <bool kIMajor>
+__device__ __forceinline__ bf16x8 operand(const bf16* T, int r0, int ks, int lane) {
+  if constexpr (!kIMajor) {
+    return ld16(T + kmaj_off(r0 + (lane & 31), 2 * ks + (lane >> 5)));
+  } else {
+    const int ka = 16 * ks + 8 * (lane >> 5);
+    return ld_tr8<kBk>(T, r0, ka, ka + 4, lane);
+  }
+}
+
+}  // namespace
+
+// C = A B^T over one 128 x 128 tile per workgroup; see the file comment.
+template <bool kAI, bool kBI, int kEpi>
+__global__ __launch_bounds__(256, 2) void proj_gemm_kernel(const ProjGemmParams p) {
+  __shared__ __align__(16) unsigned char smem_raw[kSmemBytes];
+  bf16* smem = reinterpret_cast<bf16*>(smem_raw);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int tiles_j = p.J / kTile;
+  const int64_t ti = blockIdx.x / tiles_j;
+  const int tj = (int)(blockIdx.x - ti * tiles_j);
+  const int64_t i0 = ti * kTile;
+  const int j0 = tj * kTile;
+  const int64_t nk = (p.K + kBk - 1) / kBk;
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+
+  bf16x8 ga[4], gb[4];
+  if (nk > 0) {
+    fetch_tile<kAI>(p.a, p.lda, i0, p.I, 0, p.K, tid, ga);
+    fetch_tile<kBI>(p.b, p.ldb, j0, p.J, 0, p.K, tid, gb);
+    store_tile<kAI>(smem, tid, ga);
+    store_tile<kBI>(smem + kOpElems, tid, gb);
+    __syncthreads();
+  }
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    const bool more = kt + 1 < nk;
+    if (more) {
+      fetch_tile<kAI>(p.a, p.lda, i0, p.I, (kt + 1) * kBk, p.K, tid, ga);
+      fetch_tile<kBI>(p.b, p.ldb, j0, p.J, (kt + 1) * kBk, p.K, tid, gb);
+    }
+    const bf16* TA = smem + (kt & 1) * 2 * kOpElems;
+    const bf16* TB = TA + kOpElems;
+#pragma unroll
+    for (int ks = 0; ks < kBk / 16; ++ks) {
+      bf16x8 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = operand<kAI>(TA, 64 * wm + 32 * i, ks, lane);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = operand<kBI>(TB, 64 * wn + 32 * j, ks, lane);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+    }
+    if (more) {
+      bf16* nxt = smem + ((kt + 1) & 1) * 2 * kOpElems;
+      store_tile<kAI>(nxt, tid, ga);
+      store_tile<kBI>(nxt + kOpElems, tid, gb);
+    }
+    __syncthreads();
+  }
+
+  // accumulator element v of lane l: row 8 (v/4) + 4 (l/32) + v%4, column l%32
+  if constexpr (kEpi == kProjEpiPlain) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int64_t row = i0 + 64 * wm + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          const int64_t col = j0 + 64 * wn + 32 * j + (lane & 31);
+          if (row < p.I) {
+            const int64_t at = row * p.ldc + col;
+            if (p.c_f32) {
+              float* c = static_cast<float*>(p.c);
+              c[at] = p.accumulate ? c[at] + acc[i][j][v] : acc[i][j][v];
+            } else {
+              static_cast<bf16*>(p.c)[at] = (bf16)acc[i][j][v];
+            }
+          }
+        }
+  } else {
+    // stage the tile (one head of 128 columns) in LDS, then one 16-lane row
+    // per output row: lane l16 holds dims 8 l16 .. +7, its rotation partner
+    // (dims +-64) sits in lane l16 ^ 8 of the same DPP row.
+    float* S = reinterpret_cast<float*>(smem_raw);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          S[(64 * wm + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * kStageLd + 64 * wn + 32 * j +
+            (lane & 31)] = acc[i][j][v];
+    __syncthreads();
+    const int head = tj;
+    bf16* dst;
+    int hh, nh;
+    if (head < p.hq) {
+      dst = p.q; hh = head; nh = p.hq;
+    } else if (head < p.hq + p.hkv) {
+      dst = p.k; hh = head - p.hq; nh = p.hkv;
+    } else {
+      dst = p.v; hh = head - p.hq - p.hkv; nh = p.hkv;
+    }
+    const bool rot = p.rotate && head < p.hq + p.hkv;
+    const int l16 = tid & 15, grp = tid >> 4;
+    const float sg = l16 < 8 ? -1.f : 1.f;
+    RopeFreq f[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = rot ? p.freq.f[8 * (l16 & 7) + e] : RopeFreq{0.f, 0.f};
+#pragma unroll 2
+    for (int rr = 0; rr < kTile / 16; ++rr) {
+      const int r = grp + 16 * rr;
+      const int64_t row = i0 + r;
+      const float4 x0 = *reinterpret_cast<const float4*>(S + r * kStageLd + 8 * l16);
+      const float4 x1 = *reinterpret_cast<const float4*>(S + r * kStageLd + 8 * l16 + 4);
+      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      const int ps = (rot && row < p.I) ? p.pos[row] : -1;
+      float y[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float sn = 0.f, cs = 1.f;
+        if (ps >= 0) rope_sincos(ps, f[e], sn, cs);
+        const float xp = dpp_mov<0x128>(x[e]);  // row_ror:8, the partner lane l16 ^ 8
+        y[e] = fmaf(xp, sn * sg, x[e] * cs);
+      }
+      if (row < p.I) st16(dst + (row * nh + hh) * kHeadDim + 8 * l16, pack8(y[0], y[1], y[2], y[3], y[4], y[5], y[6], y[7]));
+    }
+  }
+}
+
+namespace {
+
+__device__ __forceinline__ void load8f(const bf16* p, float (&x)[8]) {
+  const bf16x8 v = ld16(p);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = (float)v[e];
+}
+__device__ __forceinline__ void load8f(const float* p, float (&x)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+constexpr int kPackHeads = 4;  // heads loaded together, before any is used
+
+}  // namespace
+
+// dY[row] = [R(pos)^T dq[row], R(pos)^T dk[row], dv[row]] in bf16, one
+// 16-lane DPP row per token row (rows with a negative position, or every row
+// when rotate == 0, are copied unrotated).
+template <typename Src>
+__global__ __launch_bounds__(256) void proj_grad_pack_kernel(const Src* __restrict__ dq, const Src* __restrict__ dk,
+                                                             const Src* __restrict__ dv, bf16* __restrict__ dy,
+                                                             const int32_t* __restrict__ pos, int64_t rows, int hq,
+                                                             int hkv, int rotate, const RopeFreqTable freq) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
+  const int64_t r = r0 < rows ? r0 : rows - 1;  // rows past the end redo the last row and write nothing
+  const bool live = r0 < rows;
+  const int ps = rotate ? pos[r] : -1;
+  const int l = lane & 15;
+  const float sg = l < 8 ? 1.f : -1.f;
+  float cs[8], sn[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    cs[e] = 1.f;
+    sn[e] = 0.f;
+  }
+  if (ps >= 0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      rope_sincos(ps, freq.f[8 * (l & 7) + e], sn[e], cs[e]);
+      sn[e] *= sg;
+    }
+  }
+  const int heads = hq + 2 * hkv;
+  bf16* out = dy + r * (int64_t)heads * kHeadDim + 8 * l;
+  for (int h0 = 0; h0 < heads; h0 += kPackHeads) {
+    float x[kPackHeads][8];
+#pragma unroll
+    for (int u = 0; u < kPackHeads; ++u) {
+      const int h = h0 + u < heads ? h0 + u : h0;
+      const Src* src = h < hq ? dq + (r * hq + h) * kHeadDim
+                              : (h < hq + hkv ? dk + (r * hkv + (h - hq)) * kHeadDim
+                                              : dv + (r * hkv + (h - hq - hkv)) * kHeadDim);
+      load8f(src + 8 * l, x[u]);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep the loads together, ahead of their uses
+#pragma unroll
+    for (int u = 0; u < kPackHeads; ++u) {
+      const int h = h0 + u;
+      const bool turn = h < hq + hkv;
+      float y[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float xp = dpp_mov<0x128>(x[u][e]);  // row_ror:8, the partner lane l ^ 8
+        y[e] = turn ? fmaf(xp, sn[e], x[u][e] * cs[e]) : x[u][e];
+      }
+      if (live && h < heads) st16(out + (int64_t)h * kHeadDim, pack8(y[0], y[1], y[2], y[3], y[4], y[5], y[6], y[7]));
+    }
+  }
+}
+
+hipError_t launch_proj_gemm(const ProjGemmParams& p, bool a_imajor, bool b_imajor, int epi, hipStream_t stream) {
+  const int64_t tiles = ((p.I + kTile - 1) / kTile) * (p.J / kTile);
+  if (tiles <= 0) return hipSuccess;
+  const dim3 grid((unsigned)tiles), block(256);
+  if (epi == kProjEpiQkv && !a_imajor && !b_imajor)
+    hipLaunchKernelGGL((proj_gemm_kernel<false, false, kProjEpiQkv>), grid, block, 0, stream, p);
+  else if (epi == kProjEpiPlain && !a_imajor && b_imajor)
+    hipLaunchKernelGGL((proj_gemm_kernel<false, true, kProjEpiPlain>), grid, block, 0, stream, p);
+  else if (epi == kProjEpiPlain && a_imajor && b_imajor)
+    hipLaunchKernelGGL((proj_gemm_kernel<true, true, kProjEpiPlain>), grid, block, 0, stream, p);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_proj_grad_pack(const void* dq, const void* dk, const void* dv, bool src_f32, bf16* dy,
+                                 const int32_t* pos, int64_t rows, int hq, int hkv, bool rotate,
+                                 const RopeFreqTable& freq, hipStream_t stream) {
+  if (rows <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((rows * 16 + 255) / 256)), block(256);
+  if (src_f32)
+    hipLaunchKernelGGL((proj_grad_pack_kernel<float>), grid, block, 0, stream, static_cast<const float*>(dq),
+                       static_cast<const float*>(dk), static_cast<const float*>(dv), dy, pos, rows, hq, hkv,
+                       rotate ? 1 : 0, freq);
+  else
+    hipLaunchKernelGGL((proj_grad_pack_kernel<bf16>), grid, block, 0, stream, static_cast<const bf16*>(dq),
+                       static_cast<const bf16*>(dk), static_cast<const bf16*>(dv), dy, pos, rows, hq, hkv,
+                       rotate ? 1 : 0, freq);
+  return hipGetLastError();
+}
+
+}  // namespace ba
+
+// ------------------------------------------------------------------ C ABI
+
+namespace {
+
+int proj_fail(int code, const std::string& msg) {
+  ba::set_error(msg);
+  return code;
+}
+
+bool misaligned(const void* p) { return ((uintptr_t)p & 15) != 0; }
+
+// shared argument checks of the forward and backward calls
+int proj_check(int64_t rows, int32_t hidden, int32_t hq, int32_t hkv, const void* x, const void* w,
+               const int32_t* pos, float theta) {
+  if (rows < 0) return proj_fail(BA_E_INVAL, "qkv: rows must be >= 0");
+  if (hidden <= 0 || hidden % 128 != 0) return proj_fail(BA_E_UNSUPPORTED, "qkv: hidden must be a positive multiple of 128");
+  if (hq < 1 || hkv < 1 || hq % hkv != 0) return proj_fail(BA_E_INVAL, "qkv: need hq >= 1, hkv >= 1 and hq % hkv == 0");
+  if (!std::isfinite(theta) || theta < 0.f) return proj_fail(BA_E_INVAL, "qkv: theta must be finite and >= 0");
+  if ((int64_t)(hq + 2 * hkv) * ((rows + 127) / 128) > 0x7fffffffLL)
+    return proj_fail(BA_E_UNSUPPORTED, "qkv: too many output tiles for one launch");
+  if (rows > 0) {
+    if (!x || !w) return proj_fail(BA_E_INVAL, "qkv: x or w is NULL");
+    if (misaligned(x) || misaligned(w)) return proj_fail(BA_E_INVAL, "qkv: x and w must be 16-byte aligned");
+    if (theta > 0.f && !pos) return proj_fail(BA_E_INVAL, "qkv: pos is NULL with theta > 0");
+  }
+  return BA_OK;
+}
+
+ba::RopeFreqTable freq_table(float theta) {
+  ba::RopeFreqTable t{};
+  if (theta > 0.f) ba::rope_freq_table(theta, t.f);
+  return t;
+}
+
+}  // namespace
+
+extern "C" int branch_attn_qkv_workspace_size(int64_t rows, int32_t hq, int32_t hkv, size_t* bytes) {
+  if (rows < 0 || hq < 1 || hkv < 1) return proj_fail(BA_E_INVAL, "qkv workspace: need rows >= 0, hq >= 1, hkv >= 1");
+  if (!bytes) return proj_fail(BA_E_INVAL, "qkv workspace: bytes is NULL");
+  *bytes = (size_t)rows * (size_t)(hq + 2 * hkv) * ba::kHeadDim * sizeof(uint16_t);
+  return BA_OK;
+}
+
+extern "C" int branch_attn_qkv_fwd(void* stream, int64_t rows, int32_t hidden, int32_t hq, int32_t hkv,
+                                   const void* x, const void* w, const int32_t* pos, float theta, void* q,
+                                   void* k, void* v) {
+  int rc = proj_check(rows, hidden, hq, hkv, x, w, pos, theta);
+  if (rc) return rc;
+  if (rows == 0) return BA_OK;
+  if (!q || !k || !v) return proj_fail(BA_E_INVAL, "qkv: q, k or v is NULL");
+  if (misaligned(q) || misaligned(k) || misaligned(v)) return proj_fail(BA_E_INVAL, "qkv: q, k and v must be 16-byte aligned");
+  ba::ProjGemmParams p{};
+  p.a = static_cast<const ba::bf16*>(x);
+  p.b = static_cast<const ba::bf16*>(w);
+  p.lda = hidden;
+  p.ldb = hidden;
+  p.I = rows;
+  p.J = (hq + 2 * hkv) * ba::kHeadDim;
+  p.K = hidden;
+  p.q = static_cast<ba::bf16*>(q);
+  p.k = static_cast<ba::bf16*>(k);
+  p.v = static_cast<ba::bf16*>(v);
+  p.hq = hq;
+  p.hkv = hkv;
+  p.rotate = theta > 0.f ? 1 : 0;
+  p.pos = pos;
+  p.freq = freq_table(theta);
+  const hipError_t e = ba::launch_proj_gemm(p, false, false, ba::kProjEpiQkv, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return proj_fail(BA_E_HIP, std::string("qkv forward launch: ") + hipGetErrorString(e));
+  return BA_OK;
+}
+
+extern "C" int branch_attn_qkv_bwd(void* stream, int64_t rows, int32_t hidden, int32_t hq, int32_t hkv,
+                                   const void* x, const void* w, const int32_t* pos, float theta, const void* dq,
+                                   const void* dk, const void* dv, int32_t grad_dtype, void* dx, int32_t dx_dtype,
+                                   float* dw, int32_t accumulate_dw, void* workspace, size_t workspace_bytes) {
+  int rc = proj_check(rows, hidden, hq, hkv, x, w, pos, theta);
+  if (rc) return rc;
+  if (grad_dtype != BA_DTYPE_BF16 && grad_dtype != BA_DTYPE_F32)
+    return proj_fail(BA_E_INVAL, "qkv: grad_dtype must be BA_DTYPE_BF16 or BA_DTYPE_F32");
+  if (dx_dtype != BA_DTYPE_BF16 && dx_dtype != BA_DTYPE_F32)
+    return proj_fail(BA_E_INVAL, "qkv: dx_dtype must be BA_DTYPE_BF16 or BA_DTYPE_F32");
+  if (!dw || misaligned(dw)) return proj_fail(BA_E_INVAL, "qkv: dw is NULL or not 16-byte aligned");
+  if (rows > 0) {
+    if (!dq || !dk || !dv || !dx) return proj_fail(BA_E_INVAL, "qkv: dq, dk, dv or dx is NULL");
+    if (misaligned(dq) || misaligned(dk) || misaligned(dv) || misaligned(dx))
+      return proj_fail(BA_E_INVAL, "qkv: dq, dk, dv and dx must be 16-byte aligned");
+  }
+  size_t need = 0;
+  branch_attn_qkv_workspace_size(rows, hq, hkv, &need);
+  if (rows > 0 && (!workspace || workspace_bytes < need))
+    return proj_fail(BA_E_WORKSPACE, "qkv: workspace of " + std::to_string(workspace_bytes) + " bytes, need " +
+                                         std::to_string(need));
+  if (rows > 0 && ((uintptr_t)workspace & 255)) return proj_fail(BA_E_WORKSPACE, "qkv: workspace must be 256-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int32_t n = (hq + 2 * hkv) * ba::kHeadDim;
+  ba::bf16* dy = static_cast<ba::bf16*>(workspace);
+  const ba::RopeFreqTable ft = freq_table(theta);
+  hipError_t e = ba::launch_proj_grad_pack(dq, dk, dv, grad_dtype == BA_DTYPE_F32, dy, pos, rows, hq, hkv, theta > 0.f,
+                                           ft, s);
+  if (e != hipSuccess) return proj_fail(BA_E_HIP, std::string("qkv gradient pack launch: ") + hipGetErrorString(e));
+  ba::ProjGemmParams p{};
+  // dX [rows, hidden] = dY [rows, n] W [n, hidden]: A k-major, B i-major
+  p.a = dy;
+  p.lda = n;
+  p.b = static_cast<const ba::bf16*>(w);
+  p.ldb = hidden;
+  p.I = rows;
+  p.J = hidden;
+  p.K = n;
+  p.c = dx;
+  p.ldc = hidden;
+  p.c_f32 = dx_dtype == BA_DTYPE_F32;
+  p.accumulate = 0;
+  if ((e = ba::launch_proj_gemm(p, false, true, ba::kProjEpiPlain, s)) != hipSuccess)
+    return proj_fail(BA_E_HIP, std::string("qkv dX launch: ") + hipGetErrorString(e));
+  // dW [n, hidden] (+)= dY^T X: A = dY read i-major, B = X read i-major,
+  // reduction over the rows (ragged end allowed)
+  p = ba::ProjGemmParams{};
+  p.a = dy;
+  p.lda = n;
+  p.b = static_cast<const ba::bf16*>(x);
+  p.ldb = hidden;
+  p.I = n;
+  p.J = hidden;
+  p.K = rows;
+  p.c = dw;
+  p.ldc = hidden;
+  p.c_f32 = 1;
+  p.accumulate = accumulate_dw ? 1 : 0;
+  if ((e = ba::launch_proj_gemm(p, true, true, ba::kProjEpiPlain, s)) != hipSuccess)
+    return proj_fail(BA_E_HIP, std::string("qkv dW launch: ") + hipGetErrorString(e));
+  return BA_OK;
+}
