@@ -138,6 +138,115 @@ def cpu_baseline(prob, rows: int, seed: int = 1234):
                       f"all their keys, {dt:.1f} s", "seconds": round(dt, 2), "cpu": cpu}
 
 
+QKV_METRIC = "qkv projection + rotary fwd+bwd TFLOP/s (% bf16 MFMA peak), rank-share rows"
+
+
+def bench_qkv(args):
+    """Forward + backward of the QKV projection of one rank share: the main rows
+    and the branch rows projected in two calls each (the weight gradient
+    accumulated over both), positions from the plan, inputs resident in HBM.
+    FLOPs: 2 rows hidden (hq + 2 hkv) 128 per product, three products."""
+    import numpy as np
+    import torch
+    from paper_2609_07108_amd import binding as B
+    from paper_2609_07108_amd import rankshare as RS
+    from paper_2609_07108_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    prob = W.config(args.config)
+    theta = args.rope if args.rope else 5.0e5
+    hidden, hq, hkv = args.qkv_hidden, prob.hq, prob.hkv
+    share = RS.build_share(prob, materialize=False)
+    parts = [p for p in share.plan.positions(share.n_local, share.num_branch_rows) if len(p)]
+    n = (hq + 2 * hkv) * 128
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+
+    def randn(shape, scale=1.0, dtype=torch.bfloat16):
+        return (torch.randn(shape, generator=g, device="cuda") * scale).to(dtype)
+
+    w = randn((n, hidden), 1.0 / hidden ** 0.5)
+    dw = torch.empty((n, hidden), dtype=torch.float32, device="cuda")
+    io = []
+    for pos in parts:
+        r = len(pos)
+        io.append(dict(x=randn((r, hidden)), pos=torch.as_tensor(pos, dtype=torch.int32, device="cuda"),
+                       q=torch.empty((r, hq, 128), dtype=torch.bfloat16, device="cuda"),
+                       k=torch.empty((r, hkv, 128), dtype=torch.bfloat16, device="cuda"),
+                       v=torch.empty((r, hkv, 128), dtype=torch.bfloat16, device="cuda"),
+                       dq=randn((r, hq, 128)), dk=randn((r, hkv, 128)), dv=randn((r, hkv, 128)),
+                       dx=torch.empty((r, hidden), dtype=torch.bfloat16, device="cuda")))
+    ws = torch.empty(max(B.branch_attn_qkv_workspace_size(max(len(p) for p in parts), hq, hkv), 256),
+                     dtype=torch.uint8, device="cuda")
+    rows = sum(len(p) for p in parts)
+    flops = 2.0 * rows * hidden * n  # one product
+    ev = HipEvents()
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def fwd():
+        for t in io:
+            B.branch_attn_qkv_fwd(t["x"], w, hq, hkv, t["pos"], theta, t["q"], t["k"], t["v"])
+
+    def bwd():
+        for i, t in enumerate(io):
+            B.branch_attn_qkv_bwd(t["x"], w, hq, hkv, t["pos"], theta, t["dq"], t["dk"], t["dv"], t["dx"], dw,
+                                  i > 0, ws)
+
+    for _ in range(args.warmup):
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    marks = [[ev.create() for _ in range(3)] for _ in range(args.steps)]
+    for m in marks:
+        ev.record(m[0], stream)
+        fwd()
+        ev.record(m[1], stream)
+        bwd()
+        ev.record(m[2], stream)
+    torch.cuda.synchronize()
+    fwd_ms = sum(ev.ms(m[0], m[1]) for m in marks) / args.steps
+    bwd_ms = sum(ev.ms(m[1], m[2]) for m in marks) / args.steps
+    step_ms = fwd_ms + bwd_ms
+    print(f"[bench] qkv {args.steps} steps: fwd {fwd_ms:.3f} ms ({flops / fwd_ms / 1e9:.0f} TFLOP/s), "
+          f"bwd {bwd_ms:.3f} ms ({2 * flops / bwd_ms / 1e9:.0f} TFLOP/s)", file=sys.stderr, flush=True)
+
+    cpu = None
+    if args.cpu_rows > 0:
+        from oracle import qkv as OQ
+        sample = 1024 * args.cpu_rows  # about 10 s of fp64 BLAS on 16 cores at the default
+        rng = np.random.default_rng(3)
+        x = rng.standard_normal((sample, hidden))
+        wn = w.float().cpu().numpy().astype(np.float64)
+        pos = rng.integers(0, 262144, sample)
+        dq, dk, dv = (rng.standard_normal((sample, h, 128)) for h in (hq, hkv, hkv))
+        t0 = time.perf_counter()
+        OQ.forward(x, wn, hq, hkv, pos, theta)
+        OQ.backward(x, wn, hq, hkv, pos, theta, dq, dk, dv)
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(3 * 2.0 * sample * hidden * n / dt / 1e12, 4), "unit": "TFLOP/s",
+               "cores": os.cpu_count(), "kind": "oracle",
+               "sample": f"{sample} rows, fp64 forward + backward, {dt:.1f} s"}
+
+    achieved = flops / (fwd_ms / 1e3) / 1e12
+    value = 3 * flops / (step_ms / 1e3) / 1e12
+    line = {
+        "metric": QKV_METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(step_ms, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"qkv-{prob.name}", "rows": rows, "calls": [len(p) for p in parts],
+                   "hidden": hidden, "hq": hq, "hkv": hkv, "rope_theta": theta},
+        "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "ms": {"fwd": round(fwd_ms, 3), "bwd": round(bwd_ms, 3)},
+        "roofline": {"kernel": "proj_gemm_kernel (forward, rotary epilogue)", "bound": "mfma",
+                     "achieved": round(achieved, 2), "peak": round(PEAK_BF16_TFLOPS, 1), "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "launches_per_step": len(parts), "launch_ms": round(fwd_ms / len(parts), 3)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -151,6 +260,10 @@ def main():
     ap.add_argument("--rope", type=float, default=0.0, metavar="THETA",
                     help="rotate queries and keys by their positions (rotary embedding, base THETA) "
                          "in front of the attention; 0 (default) leaves them as they are")
+    ap.add_argument("--qkv-hidden", type=int, default=0, metavar="HIDDEN",
+                    help="instead of the attention step, time the grouped-query QKV projection with rotary "
+                         "embedding (forward + backward) of the workload's main and branch rows from HIDDEN "
+                         "features (its own JSON line)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB mebibytes (HBM counter calibration)")
     args = ap.parse_args()
@@ -168,6 +281,10 @@ def main():
         print(json.dumps({"error": "this build evaluates one context-parallel rank share on ONE GPU; "
                                    "--gpus > 1 is not supported (the ring exchange is not implemented)"}))
         sys.exit(2)
+
+    if args.qkv_hidden:
+        bench_qkv(args)
+        return
 
     import torch
     from paper_2609_07108_amd import binding as B
