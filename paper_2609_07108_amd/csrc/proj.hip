@@ -20,8 +20,8 @@
 // ([i][k], "k-major") or with its row index contiguous ([k][i], "i-major").
 // A workgroup of four wavefronts computes one tile, each wavefront a 64 x 64
 // quarter as 2 x 2 v_mfma_f32_32x32x16_bf16 accumulators.  Operands move
-// global -> registers -> LDS while the previous stage is multiplied (the
-// loads of stage t+1 are in flight during the MFMAs of stage t).
+// global -> registers -> LDS through two register sets, so the loads of
+// stage t+2 are in flight during the MFMAs of stage t.
 #include <cmath>
 #include <string>
 
@@ -42,57 +42,104 @@ constexpr int kSmemBytes = (4 * kOpElems * 2 > kTile * kStageLd * 4) ? 4 * kOpEl
 // eight 16-byte chunks of row r are XOR-permuted by (r/2) % 8, so that the
 // 16 lanes of an MFMA operand read (16 consecutive rows, one chunk) and of a
 // tile store (two rows, eight chunks) touch 16 distinct 16-byte bank groups.
+// i-major operand tile: 64 reduction rows x 128 columns as a plane tile
+// (tile_off), read with transposed 8-byte reads.
 __device__ __forceinline__ int kmaj_off(int r, int chunk) { return r * kBk + ((chunk ^ ((r >> 1) & 7)) << 3); }
 
-// Global -> register fetch of one operand tile, four 16-byte loads per thread.
-// k-major ([i][k], ld elements per stored row): thread t takes chunk t % 8 of
-// rows t/8 + 32q; rows past the end re-read the last row (their results are
-// never stored).  The caller guarantees the reduction slice lies inside K.
-// i-major ([k][i]): thread t takes columns 8 (t % 16) .. +7 of reduction rows
-// t/16 + 16q; rows at or past K read row K-1 and become zeros, so a ragged
-// reduction end contributes nothing.
+// Per-lane LDS byte offsets inside one operand tile, computed once: every
+// operand read, transposed read and tile store of the main loop is one of
+// these plus a compile-time constant (folded into the instruction), since
+// the XOR terms of both layouts depend on the lane alone.
+//   operand of rows r0.. (r0 % 32 == 0) at reduction step ks:
+//     k-major: rd[ks] + 128 r0;  i-major: tlo / thi + 1024 ks + 128 r0
+//   store of fetch q: st + 4096 q (k-major) or st + 1024 q (i-major)
 template <bool kIMajor>
-__device__ __forceinline__ void fetch_tile(const bf16* __restrict__ base, int64_t ld, int64_t i0, int64_t ni,
-                                           int64_t k0, int64_t nk, int tid, bf16x8 (&g)[4]) {
+struct LaneOfs {
+  uint32_t rd[4], tlo, thi, st;
+  __device__ __forceinline__ explicit LaneOfs(int tid) {
+    const int lane = tid & 63, h = lane >> 5;
+    if constexpr (!kIMajor) {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) rd[ks] = 2u * (uint32_t)kmaj_off(lane & 31, 2 * ks + h);
+      tlo = thi = 0;
+      st = 2u * (uint32_t)kmaj_off(tid >> 3, tid & 7);
+    } else {
+      const int i = lane & 15, col = (lane & 16) + 4 * (i & 3);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) rd[ks] = 0;
+      tlo = 2u * (uint32_t)tile_off<kBk>(8 * h + (i >> 2), col);
+      thi = 2u * (uint32_t)tile_off<kBk>(8 * h + 4 + (i >> 2), col);
+      st = 2u * (uint32_t)tile_off<kBk>(tid >> 4, 8 * (tid & 15));
+    }
+  }
+};
+
+template <bool kIMajor, int kR0, int kKs>
+__device__ __forceinline__ bf16x8 operand(uint32_t tile, const LaneOfs<kIMajor>& o) {
   if constexpr (!kIMajor) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      int64_t row = i0 + (tid >> 3) + 32 * q;
-      row = row < ni ? row : ni - 1;
-      g[q] = ld16(base + row * ld + k0 + 8 * (tid & 7));
-    }
+    return lds_ld16(tile + o.rd[kKs] + 128u * kR0);
   } else {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int64_t kk = k0 + (tid >> 4) + 16 * q;
-      const bf16x8 v = ld16(base + (kk < nk ? kk : nk - 1) * ld + i0 + 8 * (tid & 15));
-      g[q] = kk < nk ? v : bf16x8{};
-    }
+    const uint32_t c = 1024u * kKs + 128u * kR0;
+    const bf16x4 lo = lds_ld_tr4(tile + o.tlo + c), hi = lds_ld_tr4(tile + o.thi + c);
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   }
 }
 
 template <bool kIMajor>
-__device__ __forceinline__ void store_tile(bf16* T, int tid, const bf16x8 (&g)[4]) {
+__device__ __forceinline__ void store_tile(uint32_t tile, const LaneOfs<kIMajor>& o, const bf16x8 (&g)[4]) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    if constexpr (!kIMajor)
-      st16(T + kmaj_off((tid >> 3) + 32 * q, tid & 7), g[q]);
-    else
-      st16(T + tile_off<kBk>((tid >> 4) + 16 * q, 8 * (tid & 15)), g[q]);
-  }
+  for (int q = 0; q < 4; ++q)
+    *(__attribute__((address_space(3))) bf16x8*)(uintptr_t)(tile + o.st + (kIMajor ? 1024u : 4096u) * q) = g[q];
 }
 
-// MFMA operand for rows r0 .. r0+31 of a tile at reduction step ks (16
-// values): lane l takes row r0 + l%32, values 16 ks + 8 (l/32) .. +7.
+// Global side of one operand: per-lane 32-bit byte offsets from a
+// wave-uniform base that advances by one stage per iteration.
+// k-major ([i][k], ld elements per row): thread t fetches chunk t % 8 of
+// tile rows t/8 + 32q; rows past the end re-read the last row (their results
+// are never stored); stage kt starts at base + i0 ld + 64 kt.  The
+// reduction slices lie inside K (K % 64 == 0).
+// i-major ([k][i]): thread t fetches columns 8 (t % 16) .. +7 of reduction
+// rows t/16 + 16q; stage kt starts at base + 64 kt ld + i0.  Rows at or
+// past K (a ragged last stage only) read row K-1 and become zeros.
 template <bool kIMajor>
-__device__ __forceinline__ bf16x8 operand(const bf16* T, int r0, int ks, int lane) {
-  if constexpr (!kIMajor) {
-    return ld16(T + kmaj_off(r0 + (lane & 31), 2 * ks + (lane >> 5)));
-  } else {
-    const int ka = 16 * ks + 8 * (lane >> 5);
-    return ld_tr8<kBk>(T, r0, ka, ka + 4, lane);
+struct Fetch {
+  const char* base;  // stage 0
+  int64_t stage;     // bytes per stage
+  uint32_t off[4];
+  __device__ __forceinline__ Fetch(const bf16* a, int64_t ld, int64_t i0, int64_t ni, int tid) {
+    if constexpr (!kIMajor) {
+      base = reinterpret_cast<const char*>(a + i0 * ld);
+      stage = 2 * kBk;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        int64_t r = i0 + (tid >> 3) + 32 * q;
+        r = (r < ni ? r : ni - 1) - i0;
+        off[q] = (uint32_t)(2 * (r * ld + 8 * (tid & 7)));
+      }
+    } else {
+      base = reinterpret_cast<const char*>(a + i0);
+      stage = 2 * kBk * ld;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) off[q] = (uint32_t)(2 * (((tid >> 4) + 16 * q) * ld + 8 * (tid & 15)));
+    }
   }
-}
+  __device__ __forceinline__ void load(int64_t kt, bf16x8 (&g)[4]) const {
+    const char* b = base + kt * stage;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) g[q] = *reinterpret_cast<const bf16x8*>(b + off[q]);
+  }
+  // i-major only: the last stage when it reaches past K
+  __device__ __forceinline__ void load_tail(int64_t kt, int64_t K, int64_t ld, int tid, bf16x8 (&g)[4]) const {
+    const char* b = base + kt * stage;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t kk = kt * kBk + (tid >> 4) + 16 * q;
+      const int64_t back = kk < K ? 0 : kk - (K - 1);  // rows to step back to reach row K-1
+      const bf16x8 v = *reinterpret_cast<const bf16x8*>(b + off[q] - 2 * back * ld);
+      g[q] = kk < K ? v : bf16x8{};
+    }
+  }
+};
 
 }  // namespace
 
@@ -116,40 +163,65 @@ __global__ __launch_bounds__(256, 2) void proj_gemm_kernel(const ProjGemmParams 
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
-  bf16x8 ga[4], gb[4];
+  const LaneOfs<kAI> oa(tid);
+  const LaneOfs<kBI> ob(tid);
+  const Fetch<kAI> fa(p.a, p.lda, i0, p.I, tid);
+  const Fetch<kBI> fb(p.b, p.ldb, j0, p.J, tid);
+  const uint32_t lds0 = lds_addr(smem);
+  constexpr uint32_t kOpBytes = 2u * kOpElems;
+  // the stage that reaches past a ragged reduction end (i-major operands only)
+  const int64_t tail = (p.K % kBk) ? nk - 1 : nk;
+  auto fetch = [&](int64_t kt, bf16x8 (&ga)[4], bf16x8 (&gb)[4]) {
+    if (kt != tail) {
+      fa.load(kt, ga);
+      fb.load(kt, gb);
+    } else {
+      if constexpr (kAI) fa.load_tail(kt, p.K, p.lda, tid, ga); else fa.load(kt, ga);
+      if constexpr (kBI) fb.load_tail(kt, p.K, p.ldb, tid, gb); else fb.load(kt, gb);
+    }
+  };
+
+  // Two register sets: while stage t is multiplied, the loads of stage
+  // t + 2 are in flight into one set and the other set (stage t + 1, loaded
+  // during the previous stage) is written to the free LDS buffer afterwards,
+  // so every load has two stages of MFMA work to arrive.
+  bf16x8 ga0[4], gb0[4], ga1[4], gb1[4];
   if (nk > 0) {
-    fetch_tile<kAI>(p.a, p.lda, i0, p.I, 0, p.K, tid, ga);
-    fetch_tile<kBI>(p.b, p.ldb, j0, p.J, 0, p.K, tid, gb);
-    store_tile<kAI>(smem, tid, ga);
-    store_tile<kBI>(smem + kOpElems, tid, gb);
+    fetch(0, ga0, gb0);
+    store_tile<kAI>(lds0, oa, ga0);
+    store_tile<kBI>(lds0 + kOpBytes, ob, gb0);
     __syncthreads();
   }
-  for (int64_t kt = 0; kt < nk; ++kt) {
-    const bool more = kt + 1 < nk;
-    if (more) {
-      fetch_tile<kAI>(p.a, p.lda, i0, p.I, (kt + 1) * kBk, p.K, tid, ga);
-      fetch_tile<kBI>(p.b, p.ldb, j0, p.J, (kt + 1) * kBk, p.K, tid, gb);
-    }
-    const bf16* TA = smem + (kt & 1) * 2 * kOpElems;
-    const bf16* TB = TA + kOpElems;
-#pragma unroll
-    for (int ks = 0; ks < kBk / 16; ++ks) {
-      bf16x8 a[2], b[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = operand<kAI>(TA, 64 * wm + 32 * i, ks, lane);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = operand<kBI>(TB, 64 * wn + 32 * j, ks, lane);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
-    }
-    if (more) {
-      bf16* nxt = smem + ((kt + 1) & 1) * 2 * kOpElems;
-      store_tile<kAI>(nxt, tid, ga);
-      store_tile<kBI>(nxt + kOpElems, tid, gb);
+  // The fetches are unconditional (past the end they re-read the last stage,
+  // which is never stored): with a skipped fetch on some path, the compiler's
+  // wait counts at the stores would have to cover the newer loads as well.
+  if (nk > 0) fetch(nk > 1 ? 1 : 0, ga1, gb1);
+  auto iterate = [&](int64_t kt, const bf16x8 (&ca)[4], const bf16x8 (&cb)[4], bf16x8 (&na)[4],
+                     bf16x8 (&nb)[4]) {
+    fetch(kt + 2 < nk ? kt + 2 : nk - 1, na, nb);
+    const uint32_t TA = lds0 + (uint32_t)(kt & 1) * 2u * kOpBytes;
+    const uint32_t TB = TA + kOpBytes;
+    static_for<kBk / 16>([&](auto ks) {
+      constexpr int kKs = decltype(ks)::value;
+      const bf16x8 a0 = operand<kAI, 0, kKs>(TA + 128u * 64 * wm, oa);
+      const bf16x8 a1 = operand<kAI, 32, kKs>(TA + 128u * 64 * wm, oa);
+      const bf16x8 b0 = operand<kBI, 0, kKs>(TB + 128u * 64 * wn, ob);
+      const bf16x8 b1 = operand<kBI, 32, kKs>(TB + 128u * 64 * wn, ob);
+      acc[0][0] = mfma32(a0, b0, acc[0][0]);
+      acc[0][1] = mfma32(a0, b1, acc[0][1]);
+      acc[1][0] = mfma32(a1, b0, acc[1][0]);
+      acc[1][1] = mfma32(a1, b1, acc[1][1]);
+    });
+    if (kt + 1 < nk) {
+      const uint32_t nxt = lds0 + (uint32_t)((kt + 1) & 1) * 2u * kOpBytes;
+      store_tile<kAI>(nxt, oa, ca);
+      store_tile<kBI>(nxt + kOpBytes, ob, cb);
     }
     __syncthreads();
+  };
+  for (int64_t kt = 0; kt < nk; kt += 2) {
+    iterate(kt, ga1, gb1, ga0, gb0);
+    if (kt + 1 < nk) iterate(kt + 1, ga0, gb0, ga1, gb1);
   }
 
   // accumulator element v of lane l: row 8 (v/4) + 4 (l/32) + v%4, column l%32
@@ -214,7 +286,7 @@ __global__ __launch_bounds__(256, 2) void proj_gemm_kernel(const ProjGemmParams 
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float sn = 0.f, cs = 1.f;
-        if (ps >= 0) rope_sincos(ps, f[e], sn, cs);
+        if (ps >= 0) rope_sincos_fast(ps, f[e], sn, cs);
         const float xp = dpp_mov<0x128>(x[e]);  // row_ror:8, the partner lane l16 ^ 8
         y[e] = fmaf(xp, sn * sg, x[e] * cs);
       }
