@@ -10,7 +10,8 @@ either end of the ring, an empty sequence, sequences without branches, fp32
 gradient output, all-equal scores (Q = 0), and the mask variants of the
 draft families: DFlash/DSpark blocks of other sizes and several per window,
 DFlash with main queries, EAGLE depth per sequence up to the 64-member
-maximum.
+maximum, and rings of 16 and of the maximum 32 blocks (a middle rank and
+the last rank).
 """
 
 import numpy as np
@@ -57,6 +58,15 @@ def case(name):
     if name == "gqa_g64":
         return W.custom([512, 256], [("eagle", 2), None], hq=64, hkv=1, cp_size=2, cp_rank=1, seed=209,
                         name=name)
+    if name == "cp16":
+        # 16 ring steps, a middle rank, chunks of 16 to 64 tokens
+        return W.custom([1024, 2048, 512], [("eagle", 3), ("dflash", 16, 64), None], hq=8, hkv=2, cp_size=16,
+                        cp_rank=5, seed=210, name=name)
+    if name == "cp32_max":
+        # the largest ring the kernel arguments hold (32 blocks), the last
+        # rank (its two chunks are the middle of each sequence)
+        return W.custom([2048, 1024], [("eagle", 2), ("dflash", 8, 32)], hq=4, hkv=4, cp_size=32, cp_rank=31,
+                        seed=211, name=name)
     raise KeyError(name)
 
 
@@ -89,6 +99,8 @@ def test_config1_forward_every_rank(cuda, mode, r):
     ("mask_variants", "depth", torch.bfloat16),
     ("gqa_g3", "group", torch.bfloat16),
     ("gqa_g64", "depth", torch.float32),
+    ("cp16", "group", torch.bfloat16),
+    ("cp32_max", "depth", torch.float32),
 ])
 def test_forward_backward_parity(cuda, mode, name, layout, grad_dtype):
     prob = case(name)

@@ -172,3 +172,19 @@ def test_rope_positions_must_fit_float():
         plan.set_rope(1.0e4)
     assert e.value.code == B.BA_E_UNSUPPORTED
     assert plan.workspace_size(B.BA_MODE_PER_STEP) == before  # left without rotation
+
+
+def test_device_calls_reject_more_than_32_ring_steps():
+    """A plan may describe any CP size, but the ring-step block pointers of
+    one call must fit the kernel arguments (32): the device entry points
+    refuse larger rings before touching the GPU."""
+    import ctypes
+    C = 33
+    plan = B.Plan([0, 4 * C], [1], C, 0, 1, 1, 128, 0.088, np.zeros((0, 6), np.int32), 0)
+    fake = 0x10000  # aligned, never dereferenced: the call stops at validation
+    ptrs = (ctypes.c_void_p * C)(*([fake] * C))
+    io = B.BaFwdIO(fake, fake, fake, fake, ptrs, ptrs, fake, fake, fake, fake, None, None)
+    rc = B.lib().branch_attn_fwd(None, plan.handle, B.BA_MODE_PER_STEP, ctypes.byref(io), ctypes.c_void_p(fake),
+                                 1 << 40)
+    assert rc == B.BA_E_UNSUPPORTED
+    assert b"32" in B.lib().branch_attn_last_error()
