@@ -48,8 +48,9 @@ __device__ __forceinline__ int kmaj_off(int r, int chunk) { return r * kBk + ((c
 
 // Per-lane LDS byte offsets inside one operand tile, computed once: every
 // operand read, transposed read and tile store of the main loop is one of
-// these plus a compile-time constant (folded into the instruction), since
-// the XOR terms of both layouts depend on the lane alone.
+// these plus a compile-time constant (the instruction's offset field takes
+// it for row reads and stores; transposed reads still pay one add each),
+// since the XOR terms of both layouts depend on the lane alone.
 //   operand of rows r0.. (r0 % 32 == 0) at reduction step ks:
 //     k-major: rd[ks] + 128 r0;  i-major: tlo / thi + 1024 ks + 128 r0
 //   store of fetch q: st + 4096 q (k-major) or st + 1024 q (i-major)
