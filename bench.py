@@ -278,8 +278,9 @@ def main():
         print(json.dumps({"calibration": "copy", "bytes_read": n * 4, "bytes_written": n * 4}))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build evaluates one context-parallel rank share on ONE GPU; "
-                                   "--gpus > 1 is not supported (the ring exchange is not implemented)"}))
+        print(json.dumps({"error": "the benchmark evaluates one context-parallel rank share on ONE GPU; "
+                                   "--gpus > 1 is not supported (the ring exchange between GPUs is not "
+                                   "implemented)"}))
         sys.exit(2)
 
     if args.qkv_hidden:
