@@ -5,9 +5,10 @@
  * Co-Training for Speculative Decoding in Large-Scale, Long-Context RL
  * Post-Training"): every branch query attends (a) a causal prefix of its main
  * sequence, which is sharded over CP ranks with the packed zigzag ring, and
- * (b) the branch-local keys kept on the rank that owns the branch's anchor.
- * The two partial results are merged with the log-sum-exp rule (Eq. lse-merge).
- * The backward pass replays the same ring and accumulates gradients locally.
+ * (b) its own branch's keys, which never leave the rank holding the anchor
+ * token.  Both parts are attended separately and combined by log-sum-exp
+ * rescaling (Eq. lse-merge).  For gradients the ring is walked a second time
+ * and every rank sums its contributions in place (Sec. 3.2).
  *
  * This library evaluates ONE rank's share on one GPU.  The KV blocks that a
  * real ring would deliver step by step (one per rank) are all resident in
@@ -73,7 +74,7 @@ extern "C" {
  * row0 + i * row_stride, i = 0..len-1.  The branch's causal main prefix is the
  * main keys of sequence `seq` at positions 0..anchor (inclusive).  A group
  * must be anchored in a chunk owned by the evaluated rank (Sec. 3.2: branch
- * keys are kept on the rank that owns the anchor). */
+ * keys stay with the rank that holds the anchor token). */
 typedef struct ba_group {
   int32_t seq;
   int32_t anchor;
@@ -277,8 +278,9 @@ int lse_merge(void* stream, int64_t rows, int32_t heads, int32_t head_dim, float
 
 /* ------------------------------------------- QKV projection (draft layer)
  *
- * The step in front of the op inside a draft layer (Sec. 3.2 builds the
- * draft's attention on the target's decoder layer): grouped-query projection
+ * The step in front of the op inside a draft layer (the paper gives no
+ * projection detail; this library reads the draft layer as a Llama-style
+ * decoder layer, its own reading): grouped-query projection
  * of hidden states to q-, k- and v-heads, with the rotary embedding of
  * branch_attn_plan_set_rope applied to the queries and keys.  Plan-free: the
  * caller projects the main rows and the branch rows in separate calls, with

@@ -3,8 +3,8 @@ in front of branch attention inside a draft layer.
 
 Test infrastructure only (see the package docstring).
 
-The draft layer (Sec. 3.2: the draft's attention is built on the target's
-decoder layer) projects hidden states x [rows, hidden] with one fused linear
+The draft layer (the paper gives no projection detail; reading R20 of the
+design notes takes it to be a Llama-style decoder layer) projects hidden states x [rows, hidden] with one fused linear
 weight w [(hq + 2 hkv) d, hidden] (output-major, as a linear layer stores it):
 y = x w^T, whose consecutive d-column blocks are the hq query heads, then the
 hkv key heads, then the hkv value heads.  Queries and keys are then rotated

@@ -1,6 +1,6 @@
 // Backward branch attention for one context-parallel rank share (Sec. 3.2:
-// the backward pass replays the same KV ring and accumulates gradients
-// locally).
+// the gradients walk the KV ring a second time and each rank sums its
+// contributions where it is).
 //
 // With the final LSE of every row the probabilities of any key subset are
 // P = exp(S - LSE), so the merge of Eq. lse-merge needs no explicit backward:

@@ -1,9 +1,10 @@
 // Grouped-query QKV projection of a draft layer's attention input, with the
 // rotary embedding of the queries and keys applied in the projection's
 // epilogue, and its backward.  This is the step in front of branch attention
-// inside a draft layer (Sec. 3.2 builds the draft's attention on the target's
-// decoder layer: hidden states are projected to q-heads and fewer kv-heads,
-// queries and keys rotated by their positions, then attended).
+// inside a draft layer.  The paper gives no projection detail; this library
+// reads the draft layer as a Llama-style decoder layer (its own reading):
+// hidden states are projected to q-heads and fewer kv-heads, queries and keys
+// rotated by their positions, then attended.
 //
 //   forward:  Y = X W^T, X [rows, hidden], W [(hq + 2 hkv) * 128, hidden]
 //             (the fused q/k/v weight of a linear layer, output-major);
