@@ -31,11 +31,11 @@ from tests import gpu_helpers as H
 
 pytestmark = pytest.mark.gpu
 
-# (config, schedule, sampled main rows, sampled branch rows); the headline
-# share (config 4) runs in both schedules, the per-step one being the
-# benchmark's launch configuration
-CASES = [(2, "per_step", 4, 8), (3, "fused", 4, 8), (4, "per_step", 12, 24), (4, "fused", 4, 8),
-         (5, "fused", 4, 8)]
+# (config, schedule, sampled main rows, sampled branch rows); every workload
+# runs in both schedules, the per-step one being the benchmark's launch
+# configuration
+CASES = [(2, "per_step", 4, 8), (2, "fused", 2, 4), (3, "per_step", 4, 8), (3, "fused", 4, 8),
+         (4, "per_step", 12, 24), (4, "fused", 4, 8), (5, "per_step", 4, 8), (5, "fused", 4, 8)]
 
 
 def sample_rows(prob, mq, bq, n_main=4, n_br=8, seed=0):
