@@ -31,7 +31,7 @@ COMMON_FLAGS = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
 # otherwise get every MFMA accumulator in the accumulation registers, with a
 # copy per softmax element; its long-lived dK/dV accumulators are pinned to
 # the accumulation registers explicitly instead.
-HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wno-inline-asm",
              "-munsafe-fp-atomics", "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
@@ -52,16 +52,38 @@ def _run(cmd):
         print(text, file=sys.stderr)
 
 
+def compiler_version() -> str:
+    r = subprocess.run([hipcc(), "--version"], stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    return next((l.strip() for l in r.stdout.splitlines() if "clang version" in l), r.stdout.strip())
+
+
+# The compiler whose output was last checked by hand as well as by the hazard
+# check below.  Another version still builds (the check runs on whatever it
+# generates) but says so.
+VERIFIED_COMPILER = "AMD clang version 22.0.0git (https://github.com/RadeonOpenCompute/llvm-project roc-7.2.0 26014"
+
+
 def build(verbose: bool = False, jobs: int = 4) -> str:
-    """Compile every source and link the shared library; returns its path."""
+    """Compile every source and link the shared library; returns its path.
+
+    The device assembly of every source is kept (``-save-temps``) and run
+    through :mod:`hazards`: the inline-assembly MFMAs and direct loads carry
+    wait-state requirements that the compiler does not pad, and a build whose
+    generated code breaks one is refused."""
+    from . import hazards
+
     os.makedirs(OUT_DIR, exist_ok=True)
     cc = hipcc()
+    ver = compiler_version()
+    if not ver.startswith(VERIFIED_COMPILER):
+        print(f"note: compiler {ver!r} differs from the one the kernels' schedules were last read under; "
+              f"relying on the generated-code hazard check", file=sys.stderr)
     tmp = tempfile.mkdtemp(prefix="ba_build_", dir=OUT_DIR)
     try:
         objs, procs = [], []
         for src in HIP_SOURCES + HOST_SOURCES:
             obj = os.path.join(tmp, os.path.splitext(src)[0] + ".o")
-            cmd = [cc] + COMMON_FLAGS + (HIP_FLAGS if src.endswith(".hip") else []) + \
+            cmd = [cc] + COMMON_FLAGS + (HIP_FLAGS + ["-save-temps=obj"] if src.endswith(".hip") else []) + \
                 ["-c", os.path.join(CSRC, src), "-o", obj]
             if verbose:
                 print(" ".join(cmd))
@@ -77,6 +99,14 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
                 raise RuntimeError(f"compile failed ({' '.join(cmd)}):\n{text}")
             if text.strip():
                 print(text, file=sys.stderr)
+        errs = []
+        for src in HIP_SOURCES:
+            asm = os.path.join(tmp, f"{os.path.splitext(src)[0]}-hip-amdgcn-amd-amdhsa-{ARCH}.s")
+            if not os.path.exists(asm):
+                raise RuntimeError(f"device assembly of {src} missing ({asm}): cannot run the hazard check")
+            errs += hazards.check_file(asm)
+        if errs:
+            raise RuntimeError("hazard check failed on the generated code:\n" + "\n".join(errs[:40]))
         lib_tmp = os.path.join(tmp, LIB_NAME)
         _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", lib_tmp] + objs)
         dst = os.path.join(OUT_DIR, LIB_NAME)

@@ -56,9 +56,14 @@ __device__ __forceinline__ void mfma32_v(f32x16& d, const bf16x8& a, const bf16x
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "a"(b));
 }
 // mfma32_v_first with the accumulation starting from c (vector registers);
-// s_nop 1 pads an addend just written by a vector instruction.
+// s_nop 1 pads an addend just written by a vector instruction (kPad false:
+// the addend was written long before, e.g. a loop-invariant value).
+template <bool kPad = true>
 __device__ __forceinline__ void mfma32_v_init(f32x16& d, const bf16x8& a, const bf16x8& b, const f32x16& c) {
-  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
+  if constexpr (kPad)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
+  else
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
 }
 
 // 16-byte global load straight into accumulation registers (for MFMA
@@ -200,13 +205,15 @@ __device__ __forceinline__ const void* uniform_ptr(const void* p) {
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
   return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
 }
+// (a direct load reads M0 one wait state after a scalar write of it at the
+// earliest: the s_nop 0 between them is that wait state)
 __device__ __forceinline__ void dma16_async(const void* base, uint32_t off, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base),
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base),
                "s"(__builtin_amdgcn_readfirstlane(lds_addr))
                : "memory", "m0");
 }
 __device__ __forceinline__ void dma4_async(const void* base, uint32_t off, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(off), "s"(base),
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1" ::"v"(off), "s"(base),
                "s"(__builtin_amdgcn_readfirstlane(lds_addr))
                : "memory", "m0");
 }
