@@ -652,7 +652,7 @@ __global__ __launch_bounds__(256) void bwd_kv_reduce_kernel(BwdParams p) {
 namespace {
 
 constexpr int kDqBufs = 3;
-constexpr int kDqAhead = 2;  // operand fragments read ahead of their MFMAs (two MFMAs each)
+constexpr int kDqAhead = 3;  // operand fragments read ahead of their MFMAs (two MFMAs each)
 
 // Element e of a key block (32 per lane): the 8-key chunk tt = e/16 (keys
 // 16 tt + 8 kb.. in the lane's accumulator slots 8 tt..), row block
@@ -786,16 +786,33 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
       asm volatile("" : "+s"(d.kb), "+s"(d.vb));
       return d;
     };
+    // a piece's byte offset: row part min(row, nrow - 1) * row stride (the
+    // clamp on the row offset itself, the stride being positive) plus the
+    // column part, both lane constants precomputed once
+    uint32_t frow[4], fcol[4];
+#pragma unroll
+    for (int m4 = 0; m4 < 4; ++m4) {
+      const int m = 4 * wave + m4;
+      frow[m4] = (uint32_t)(dma_row<kFwdKeys>(m, lane) * (int)kv_row_stride) * 2u;
+      fcol[m4] = (uint32_t)dma_col<kFwdKeys>(m, lane) * 2u;
+    }
     auto fetch_piece = [&](const DmaTile& d, int k) {
       const int m4 = k >> 1, tensor = k & 1;
       const int m = 4 * wave + m4;
-      int u = dma_row<kFwdKeys>(m, lane);
-      u = u < d.nrow ? u : d.nrow - 1;
-      const uint32_t off = (uint32_t)(u * (int)kv_row_stride + dma_col<kFwdKeys>(m, lane)) * 2u;
+      const uint32_t lim = (uint32_t)((d.nrow - 1) * (int)kv_row_stride) * 2u;  // wavefront-uniform
+      const uint32_t off = min(frow[m4], lim) + fcol[m4];
       dma16_async(tensor ? d.vb : d.kb, off, d.dst + (uint32_t)tensor * kTileBytes + dma_dst_bytes<kFwdKeys>(m));
     };
 
-    f32x16 s0[2], s1[2], p0[2], p1[2];  // S^T and dP^T of key blocks 0 and 1: [rb]
+    // -Delta of the lane's row, the starting value of the dP^T accumulations
+    // (dP^T - Delta comes out of the MFMAs)
+    f32x16 ndv[2];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) ndv[rb][v] = ndl[rb];
+
+    f32x16 s0[2], s1[2], p0[2], p1[2];  // S^T and dP^T - Delta of key blocks 0 and 1: [rb]
     u32x4 ds0[2][2], ds1[2][2];         // dS^T as bf16 pairs: [rb][tt], B operands of dQ^T
     float sv0 = 0.f, sv1 = 0.f;
 
@@ -803,7 +820,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
     auto element = [&](const f32x16 (&S)[2], const f32x16 (&P)[2], u32x4 (&D)[2][2], float& prv, int e) {
       const int tt = e >> 4, rb = (e >> 3) & 1, i = e & 7, v = 8 * tt + i;
       const float pr = fast_exp2(__builtin_fmaf(S[rb][v], p.scale_log2, nl2[rb]));
-      const float ds = pr * (P[rb][v] + ndl[rb]);
+      const float ds = pr * P[rb][v];
       if (i & 1) {
         uint32_t w = __builtin_bit_cast(uint32_t, bf16x2{(bf16)prv, (bf16)ds});
         asm volatile("" : "+v"(w));  // packed in this slot, not next to the MFMA that reads it
@@ -859,7 +876,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
           // sit right before them: padded there)
           case 1: mfma32_acc<TAIL>(dq[rb][x & 3], a, __builtin_bit_cast(bf16x8, ds1[rb][x >> 2])); break;
           case 2:
-            if (x == 0) mfma32_v_first(p0[rb], a, greg[rb][0]);
+            if (x == 0) mfma32_v_init<false>(p0[rb], a, greg[rb][0], ndv[rb]);
             else mfma32_v(p0[rb], a, greg[rb][x]);
             break;
           case 3:
@@ -867,7 +884,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
             else mfma32_v(s1[rb], a, qreg[rb][x]);
             break;
           case 4:
-            if (x == 0) mfma32_v_first(p1[rb], a, greg[rb][0]);
+            if (x == 0) mfma32_v_init<false>(p1[rb], a, greg[rb][0], ndv[rb]);
             else mfma32_v(p1[rb], a, greg[rb][x]);
             break;
           default: mfma32_acc<false>(dq[rb][x & 3], a, __builtin_bit_cast(bf16x8, ds0[rb][x >> 2])); break;

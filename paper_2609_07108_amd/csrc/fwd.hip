@@ -164,12 +164,21 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
       asm volatile("" : "+s"(d.kb), "+s"(d.vb));
       return d;
     };
+    // a piece's byte offset: row part min(row, nrow - 1) * row stride (the
+    // clamp on the row offset itself, the stride being positive) plus the
+    // column part, both lane constants precomputed once
+    uint32_t frow[4], fcol[4];
+#pragma unroll
+    for (int m4 = 0; m4 < 4; ++m4) {
+      const int m = 4 * wave + m4;
+      frow[m4] = (uint32_t)(dma_row<kFwdKeys>(m, lane) * (int)kv_row_stride) * 2u;
+      fcol[m4] = (uint32_t)dma_col<kFwdKeys>(m, lane) * 2u;
+    }
     auto fetch_piece = [&](const DmaTile& d, int k) {
       const int m4 = k >> 1, tensor = k & 1;
       const int m = 4 * wave + m4;
-      int u = dma_row<kFwdKeys>(m, lane);
-      u = u < d.nrow ? u : d.nrow - 1;
-      const uint32_t off = (uint32_t)(u * (int)kv_row_stride + dma_col<kFwdKeys>(m, lane)) * 2u;
+      const uint32_t lim = (uint32_t)((d.nrow - 1) * (int)kv_row_stride) * 2u;  // wavefront-uniform
+      const uint32_t off = min(frow[m4], lim) + fcol[m4];
       dma16_async(tensor ? d.vb : d.kb, off, d.dst + (uint32_t)tensor * kTileBytes + dma_dst_bytes<kFwdKeys>(m));
     };
     auto fetch = [&](const KvCursor& c, int buf) {
