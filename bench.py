@@ -117,9 +117,11 @@ def cpu_baseline(prob, rows: int, seed: int = 1234):
     dob = prob.draw("dob", sb).float().numpy() if len(sb) else np.zeros((0, H, d), np.float32)
     args = [t[k] for k in ("qm", "km", "vm", "qb", "kb", "vb")]
     t0 = time.perf_counter()
-    oracle.forward(prob, *args, sm, sb)
-    oracle.backward(prob, *args, dom, dob, sm, sb)
-    dt = time.perf_counter() - t0
+    ref_f = oracle.forward(prob, *args, sm, sb)
+    t1 = time.perf_counter()
+    ref_b = oracle.backward(prob, *args, dom, dob, sm, sb)
+    t2 = time.perf_counter()
+    dt, dt_f, dt_b = t2 - t0, t1 - t0, t2 - t1
     pm, pl = oracle.allowed_pair_counts(prob, sm, sb)
     f_fwd, f_bwd = oracle.useful_flops(prob, pm + pl)
     try:
@@ -133,9 +135,45 @@ def cpu_baseline(prob, rows: int, seed: int = 1234):
             cpu = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
     except OSError:
         pass
-    return {"value": (f_fwd + f_bwd) / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{len(sm)} main + {len(sb)} branch query rows of the share, fp64 fwd+bwd against "
-                      f"all their keys, {dt:.1f} s", "seconds": round(dt, 2), "cpu": cpu}
+    # the oracle materialises every key of a row's sequence, so its cost per
+    # row is about constant within a share: extrapolate by rows
+    n_rows = len(mq) + len(bq)
+    scale_rows = n_rows / max(1, len(sm) + len(sb))
+    res = {"value": (f_fwd + f_bwd) / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+           "sample": f"{len(sm)} main + {len(sb)} branch query rows of the share, fp64 fwd+bwd against "
+                     f"all their keys, {dt:.1f} s", "seconds": round(dt, 2), "cpu": cpu,
+           "cpu_ms_fwd": round(dt_f * 1e3 * scale_rows, 1), "cpu_ms_bwd": round(dt_b * 1e3 * scale_rows, 1),
+           "extrapolated": scale_rows > 1.0,
+           "extrapolation": f"x{scale_rows:.1f}: the sample's wall time scaled by rows ({n_rows} query rows)"}
+    return res, (sm, sb, ref_f, ref_b)
+
+
+def sample_parity(share, out, sample):
+    """Errors of the GPU outputs of the timed run on the CPU sample's rows
+    (O and LSE max-abs, dQ relative L2), against the oracle values the CPU
+    baseline computed on the same inputs."""
+    import numpy as np
+    import torch
+    sm, sb, ref_f, ref_b = sample
+    g2l = {int(g): i for i, g in enumerate(share.l2g)}
+    bmap = {int(g): int(l) for g, l in zip(share.br_rows_global, share.br_rows_local)}
+    mi = torch.tensor([g2l[int(g)] for g in sm], dtype=torch.long, device=out["o_main"].device)
+    bi = torch.tensor([bmap[int(g)] for g in sb], dtype=torch.long, device=out["o_main"].device)
+    f = lambda x: x.double().cpu().numpy()
+    o_err = lse_err = 0.0
+    dq, dq_ref = [], []
+    for idx, o, lse, dqg, ro, rl, rdq in ((mi, "o_main", "lse_main", "dq_main", ref_f[0], ref_f[1], ref_b["dq_main"]),
+                                          (bi, "o_br", "lse_br", "dq_br", ref_f[2], ref_f[3], ref_b["dq_br"])):
+        if len(idx) == 0:
+            continue
+        o_err = max(o_err, float(np.abs(f(out[o][idx]) - ro).max()))
+        lse_err = max(lse_err, float(np.abs(f(out[lse][:, idx]) - rl).max()))
+        dq.append(f(out[dqg][idx]).ravel())
+        dq_ref.append(rdq.ravel())
+    dq, dq_ref = np.concatenate(dq), np.concatenate(dq_ref)
+    rel = float(np.linalg.norm(dq - dq_ref) / max(np.linalg.norm(dq_ref), 1e-300))
+    return {"rows": int(len(sm) + len(sb)), "o_max_abs": o_err, "lse_max_abs": lse_err, "dq_rel_l2": rel,
+            "bars": {"o_max_abs": 2e-2, "lse_max_abs": 1e-3, "dq_rel_l2": 1e-2}}
 
 
 QKV_METRIC = "qkv projection + rotary fwd+bwd TFLOP/s (% bf16 MFMA peak), rank-share rows"
@@ -312,12 +350,19 @@ def main():
     ev = HipEvents()
     stream = torch.cuda.current_stream().cuda_stream
     fb, fe, bb, be, bk = [], [], [], [], []
+    c0, c1, c2 = [], [], []  # whole-call boundaries: before fwd, between fwd and bwd, after bwd
 
     def step(i=None):
         evf = (fb[i], fe[i]) if i is not None else (None, None)
         evb = (bb[i], be[i], bk[i]) if i is not None else (None, None, None)
+        if i is not None:
+            ev.record(c0[i], stream)
         RS.run_fwd(share, out, mode, ws, ring_events=evf)
+        if i is not None:
+            ev.record(c1[i], stream)
         RS.run_bwd(share, out, mode, ws, ring_events=evb)
+        if i is not None:
+            ev.record(c2[i], stream)
 
     for _ in range(args.warmup):
         step()
@@ -326,6 +371,8 @@ def main():
     for _ in range(args.steps):
         fb.append(ev.create()); fe.append(ev.create()); bb.append(ev.create()); be.append(ev.create())
         bk.append(ev.create())
+        c0.append(ev.create()); c1.append(ev.create()); c2.append(ev.create())
+    torch.cuda.reset_peak_memory_stats()
     start, stop = ev.create(), ev.create()
     torch.cuda.synchronize()
     ev.record(start, stream)
@@ -335,6 +382,9 @@ def main():
     torch.cuda.synchronize()
     total_ms = ev.ms(start, stop)
     ms_step = total_ms / args.steps
+    peak_mem = torch.cuda.max_memory_allocated()
+    gpu_ms_fwd = sum(ev.ms(a, b) for a, b in zip(c0, c1)) / args.steps
+    gpu_ms_bwd = sum(ev.ms(a, b) for a, b in zip(c1, c2)) / args.steps
     fwd_ring_ms = sum(ev.ms(a, b) for a, b in zip(fb, fe)) / args.steps
     bwd_ring_ms = sum(ev.ms(a, b) for a, b in zip(bb, be)) / args.steps
     # the backward ring part is two kernels: dK/dV (S, dP, dV, dK: 8d per
@@ -354,10 +404,24 @@ def main():
     achieved = dom_flops / (dom_ms / 1e3) / 1e12
     value = (f_fwd + f_bwd) / (ms_step / 1e3) / 1e12
 
-    cpu = None
+    cpu = parity = None
     if args.cpu_rows > 0:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(prob, args.cpu_rows)
+        cpu, sample = cpu_baseline(prob, args.cpu_rows)
+        parity = sample_parity(share, out, sample) if not args.rope else None
+
+    # minimum HBM traffic of one step: every input read once and every output
+    # written once (fwd: Q, K/V of every ring block, branch K/V in; O, LSE out;
+    # bwd: Q, K, V, O, dO, LSE in; dQ, dK, dV out, bf16)
+    row_q = hq * d * 2
+    row_kv = prob.hkv * d * 2
+    nq = share.plan.info()[1]  # query rows of the share (main + branch)
+    n_kv = prob.cp_size * share.n_local + share.num_branch_rows
+    alg_fwd = nq * (row_q * 2 + hq * 4) + n_kv * row_kv * 2
+    alg_bwd = nq * (row_q * 4 + hq * 4) + n_kv * row_kv * 4
+    alg_bytes = alg_fwd + alg_bwd
+    meas = [measured_traffic(k, prob.name, args.mode) for k in kern] if not args.rope else [None]
+    meas_bytes = sum(m * launches for m in meas) if all(m is not None for m in meas) else None
 
     n_local, ntok = share.plan.info()
     traffic = measured_traffic(dom_name, prob.name, args.mode) if not args.rope else None
@@ -371,7 +435,18 @@ def main():
                    "rope_theta": args.rope},
         "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "useful_tflop_per_step": {"fwd": round(f_fwd / 1e12, 3), "bwd": round(f_bwd / 1e12, 3)},
+        "gpu_ms_fwd": round(gpu_ms_fwd, 3), "gpu_ms_bwd": round(gpu_ms_bwd, 3),
         "ring_ms": {"fwd": round(fwd_ring_ms, 3), "bwd": round(bwd_ring_ms, 3)},
+        "hbm_gbps": round(alg_bytes / (ms_step / 1e3) / 1e9, 1),
+        "hbm": {"algorithmic_bytes_per_step": int(alg_bytes), "peak_gbps": PEAK_HBM_GBS,
+                "measured_bytes_per_step": meas_bytes,
+                "measured_gbps": None if meas_bytes is None else round(meas_bytes / (ms_step / 1e3) / 1e9, 1),
+                "note": "hbm_gbps: algorithmic bytes (inputs read once, outputs written once) per step time; "
+                        "measured: rocprofv3 FETCH_SIZE + WRITE_SIZE of the three ring kernels, when taken on "
+                        "the current sources"},
+        "peak_mem_gb": round(peak_mem / 1e9, 3),
+        "workspace_gb": round(ws.numel() / 1e9, 3),
+        "parity": parity,
         "kernels": {k: {"ms": round(v[0], 3), "tflops": round(v[1] / v[0] / 1e9, 1)} for k, v in kern.items()},
         "roofline": {"kernel": dom_name, "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": round(PEAK_BF16_TFLOPS, 1), "unit": "TFLOP/s",
