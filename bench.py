@@ -291,8 +291,9 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=4, help="named workload 1..5 (4 = 256K headline)")
-    ap.add_argument("--mode", choices=["fused", "per_step"], default="per_step",
-                    help="per_step: one launch per ring step (the ring's schedule); fused: one walk over all blocks")
+    ap.add_argument("--mode", choices=["auto", "fused", "per_step"], default="auto",
+                    help="per_step: one launch per ring step (the ring's schedule); fused: one walk over all "
+                         "blocks; auto (default): the plan's choice (per-step at the 256K share)")
     ap.add_argument("--cpu-rows", type=int, default=48,
                     help="query rows of the CPU oracle sample (about 12 s on 16 cores; 0 disables)")
     ap.add_argument("--rope", type=float, default=0.0, metavar="THETA",
@@ -333,9 +334,11 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     prob = W.config(args.config)
-    mode = B.BA_MODE_FUSED if args.mode == "fused" else B.BA_MODE_PER_STEP
     t0 = time.perf_counter()
     share = RS.build_share(prob, device="cuda:0", with_grad=True, rope_theta=args.rope)
+    mode = share.plan.mode({"fused": B.BA_MODE_FUSED, "per_step": B.BA_MODE_PER_STEP,
+                            "auto": B.BA_MODE_AUTO}[args.mode])
+    mode_name = "fused" if mode == B.BA_MODE_FUSED else "per_step"
     out = RS.alloc_outputs(share, grads=True)
     ws = RS.workspace(share, mode, backward=True)
     torch.cuda.synchronize()
@@ -420,16 +423,17 @@ def main():
     alg_fwd = nq * (row_q * 2 + hq * 4) + n_kv * row_kv * 2
     alg_bwd = nq * (row_q * 4 + hq * 4) + n_kv * row_kv * 4
     alg_bytes = alg_fwd + alg_bwd
-    meas = [measured_traffic(k, prob.name, args.mode) for k in kern] if not args.rope else [None]
+    meas = [measured_traffic(k, prob.name, mode_name) for k in kern] if not args.rope else [None]
     meas_bytes = sum(m * launches for m in meas) if all(m is not None for m in meas) else None
 
     n_local, ntok = share.plan.info()
-    traffic = measured_traffic(dom_name, prob.name, args.mode) if not args.rope else None
+    traffic = measured_traffic(dom_name, prob.name, mode_name) if not args.rope else None
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": prob.name, "describe": prob.describe, "mode": args.mode,
+        "config": {"workload": prob.name, "describe": prob.describe, "mode": mode_name,
+                   "mode_requested": args.mode,
                    "query_rows": ntok, "main_keys": prob.n_main, "hq": prob.hq, "hkv": prob.hkv,
                    "head_dim": d, "cp_size": prob.cp_size, "cp_rank": prob.cp_rank,
                    "rope_theta": args.rope},

@@ -65,6 +65,12 @@ extern "C" {
  *   branch-local part with Eq. lse-merge and writes the result. */
 #define BA_MODE_PER_STEP 0
 #define BA_MODE_FUSED 1
+/* BA_MODE_AUTO: the plan picks one of the two.  Per-step when every ring
+ * step's dK/dV launch has enough work items to fill the GPU on its own (1024
+ * before any splitting); fused otherwise (shares of short sequences), where
+ * per-step launches leave the GPU partly idle and pay a running-sum pass per
+ * step.  Accepted wherever a mode is. */
+#define BA_MODE_AUTO 2
 
 #define BA_MAX_GROUP_LEN 64    /* members per branch group                 */
 #define BA_HEAD_DIM 128        /* the only head_dim with kernels            */
@@ -223,6 +229,11 @@ int branch_attn_plan_set_rope(ba_plan* plan, float theta);
  * rotary embedding of branch_attn_plan_set_rope uses, and the ones to pass to
  * branch_attn_qkv_fwd / _bwd.  Either pointer may be NULL (skipped). */
 int branch_attn_plan_positions(const ba_plan* plan, int32_t* main_pos, int32_t* br_pos);
+
+/* The schedule `mode` stands for with this plan (BA_MODE_AUTO resolved;
+ * the other modes map to themselves).  Host only.  BA_E_INVAL for an unknown
+ * mode. */
+int branch_attn_plan_mode(const ba_plan* plan, int32_t mode, int32_t* resolved);
 
 /* Workspace bytes needed by branch_attn_fwd / branch_attn_bwd in `mode`. */
 int branch_attn_workspace_size(const ba_plan* plan, int32_t mode, size_t* fwd_bytes,

@@ -29,12 +29,14 @@ BA_DTYPE_BF16 = 0
 BA_DTYPE_F32 = 1
 BA_MODE_PER_STEP = 0
 BA_MODE_FUSED = 1
+BA_MODE_AUTO = 2
 
 EXPORTED = ("zigzag_partition", "branch_attn_plan_create", "branch_attn_plan_destroy",
             "branch_attn_workspace_size", "branch_attn_plan_info", "branch_attn_useful_flops",
-            "branch_attn_pair_counts", "branch_attn_last_error", "branch_attn_fwd", "branch_attn_bwd",
+            "branch_attn_pair_counts", "branch_attn_last_error", "branch_attn_fwd",
+            "branch_attn_bwd",
             "lse_merge", "branch_attn_plan_set_rope", "branch_attn_plan_positions", "branch_attn_qkv_fwd",
-            "branch_attn_qkv_bwd", "branch_attn_qkv_workspace_size")
+            "branch_attn_qkv_bwd", "branch_attn_qkv_workspace_size", "branch_attn_plan_mode")
 
 c_i32 = ctypes.c_int32
 c_vp = ctypes.c_void_p
@@ -93,6 +95,7 @@ def lib() -> ctypes.CDLL:
         L.branch_attn_plan_set_rope.argtypes = [c_vp, ctypes.c_float]
         L.branch_attn_workspace_size.argtypes = [c_vp, c_i32, ctypes.POINTER(ctypes.c_size_t),
                                                  ctypes.POINTER(ctypes.c_size_t)]
+        L.branch_attn_plan_mode.argtypes = [c_vp, c_i32, ctypes.POINTER(c_i32)]
         L.branch_attn_plan_info.argtypes = [c_vp, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
         L.branch_attn_useful_flops.argtypes = [c_vp, ctypes.POINTER(ctypes.c_double),
                                                ctypes.POINTER(ctypes.c_double)]
@@ -189,6 +192,12 @@ class Plan:
         P = ctypes.POINTER(c_i32)
         _check(lib().branch_attn_plan_positions(self._h, mp.ctypes.data_as(P), bp.ctypes.data_as(P)))
         return mp[:n_local], bp[:num_branch_rows]
+
+    def mode(self, mode: int = BA_MODE_AUTO) -> int:
+        """The schedule `mode` stands for with this plan (BA_MODE_AUTO resolved)."""
+        r = c_i32()
+        _check(lib().branch_attn_plan_mode(self._h, int(mode), ctypes.byref(r)))
+        return r.value
 
     def workspace_size(self, mode: int):
         f, b = ctypes.c_size_t(), ctypes.c_size_t()

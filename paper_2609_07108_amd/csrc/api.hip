@@ -133,6 +133,7 @@ extern "C" int branch_attn_fwd(void* stream_, const ba_plan* plan, int32_t mode,
   if (!io) return fail(BA_E_INVAL, "io is NULL");
   if (!plan) return fail(BA_E_INVAL, "plan is NULL");
   const Plan& P = plan->p;
+  mode = resolve_mode(P, mode);
   const bool has_main = P.any_main_query;   // some sequence's main tokens are queries
   const bool has_keys = P.n_local > 0;      // main keys exist
   const bool has_br = P.num_branch_rows > 0 && !P.groups.empty();
@@ -207,6 +208,7 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
   if (!io) return fail(BA_E_INVAL, "io is NULL");
   if (!plan) return fail(BA_E_INVAL, "plan is NULL");
   const Plan& P = plan->p;
+  mode = resolve_mode(P, mode);
   const bool has_main = P.any_main_query;
   const bool has_keys = P.n_local > 0;
   const bool has_br = P.num_branch_rows > 0 && !P.groups.empty();

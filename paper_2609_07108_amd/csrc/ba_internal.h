@@ -182,7 +182,14 @@ struct Plan {
   double pairs_per_head = 0.0;  // allowed (query, key) pairs per query head
   double main_pairs_per_head = 0.0;   // ... of which on the causal main prefix
   int32_t max_group_len = 0;
+  // schedule BA_MODE_AUTO resolves to: per-step when every ring step's dK/dV
+  // launch has at least kKvSplitBelow work items before splitting (the
+  // launches fill the GPU), fused otherwise
+  int32_t auto_mode = 1;
 };
+
+// BA_MODE_AUTO -> the plan's choice; other values unchanged
+inline int32_t resolve_mode(const Plan& p, int32_t mode) { return mode == BA_MODE_AUTO ? p.auto_mode : mode; }
 
 // workspace layout (byte offsets), computed from a plan
 struct WorkspaceLayout {

@@ -188,3 +188,21 @@ def test_device_calls_reject_more_than_32_ring_steps():
                                  1 << 40)
     assert rc == B.BA_E_UNSUPPORTED
     assert b"32" in B.lib().branch_attn_last_error()
+
+
+def test_auto_schedule_choice_per_plan():
+    """BA_MODE_AUTO: per-step only when every ring step's dK/dV launch fills
+    the GPU on its own (the 256K share, the 32K DFlash sequence); fused for
+    the shares of short sequences."""
+    want = {2: B.BA_MODE_FUSED, 3: B.BA_MODE_PER_STEP, 4: B.BA_MODE_PER_STEP, 5: B.BA_MODE_FUSED}
+    for cfg, mode in want.items():
+        share = RS.build_share(W.config(cfg), materialize=False)
+        assert share.plan.mode(B.BA_MODE_AUTO) == mode, cfg
+        assert share.plan.mode(B.BA_MODE_FUSED) == B.BA_MODE_FUSED
+        assert share.plan.mode(B.BA_MODE_PER_STEP) == B.BA_MODE_PER_STEP
+        assert share.plan.workspace_size(B.BA_MODE_AUTO) == share.plan.workspace_size(mode)
+    share = RS.build_share(W.config(1), materialize=False)
+    with pytest.raises(B.BranchAttnError):
+        share.plan.mode(3)
+    with pytest.raises(B.BranchAttnError):
+        share.plan.workspace_size(3)
