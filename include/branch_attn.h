@@ -267,6 +267,20 @@ const char* branch_attn_last_error(void);
 int branch_attn_fwd(void* stream, const ba_plan* plan, int32_t mode, const ba_fwd_io* io,
                     void* workspace, size_t workspace_bytes);
 
+/* branch_attn_fwd without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The scratch is a static device array of
+ * 64 MiB per GPU, held until the process ends; it covers the fused forward of
+ * every workload up to the 256K-token share (4 MiB of plan tables there),
+ * and the per-step schedule of small shares.  Allocates nothing: no
+ * hipMalloc, hipFree or allocating library call.  BA_E_WORKSPACE if the plan
+ * and mode need more scratch than that (per-step running sums of large
+ * shares, rotary-embedding copies); other errors as branch_attn_fwd.  Every
+ * call on one GPU shares that GPU's scratch: calls that overlap on one GPU
+ * (several streams or threads) race and must be serialised by the caller.
+ * Results are identical to branch_attn_fwd with the same plan and mode. */
+int branch_attn_fwd_noalloc(void* stream, const ba_plan* plan, int32_t mode, const ba_fwd_io* io);
+
 /* Backward (Sec. 3.2: the ring is replayed and gradients accumulate
  * locally): gradients of sum <dO, O> with respect to every input of the
  * rank share.  Workspace rules as for branch_attn_fwd (bwd_bytes). */

@@ -33,7 +33,7 @@ BA_MODE_AUTO = 2
 
 EXPORTED = ("zigzag_partition", "branch_attn_plan_create", "branch_attn_plan_destroy",
             "branch_attn_workspace_size", "branch_attn_plan_info", "branch_attn_useful_flops",
-            "branch_attn_pair_counts", "branch_attn_last_error", "branch_attn_fwd",
+            "branch_attn_pair_counts", "branch_attn_last_error", "branch_attn_fwd", "branch_attn_fwd_noalloc",
             "branch_attn_bwd",
             "lse_merge", "branch_attn_plan_set_rope", "branch_attn_plan_positions", "branch_attn_qkv_fwd",
             "branch_attn_qkv_bwd", "branch_attn_qkv_workspace_size", "branch_attn_plan_mode")
@@ -103,6 +103,7 @@ def lib() -> ctypes.CDLL:
                                               ctypes.POINTER(ctypes.c_double)]
         L.branch_attn_last_error.restype = ctypes.c_char_p
         L.branch_attn_fwd.argtypes = [c_vp, c_vp, c_i32, ctypes.POINTER(BaFwdIO), c_vp, ctypes.c_size_t]
+        L.branch_attn_fwd_noalloc.argtypes = [c_vp, c_vp, c_i32, ctypes.POINTER(BaFwdIO)]
         L.branch_attn_bwd.argtypes = [c_vp, c_vp, c_i32, ctypes.POINTER(BaBwdIO), c_vp, ctypes.c_size_t]
         L.lse_merge.argtypes = [c_vp, ctypes.c_int64, c_i32, c_i32, c_vp, c_vp, c_vp, c_i32, c_vp]
         L.branch_attn_plan_positions.argtypes = [c_vp, ctypes.POINTER(c_i32), ctypes.POINTER(c_i32)]
@@ -229,6 +230,15 @@ def branch_attn_fwd(plan: Plan, mode: int, q_main, q_br, k_br, v_br, k_step, v_s
                  _ptr(lse_main), _ptr(lse_br), ring_events[0], ring_events[1])
     _check(lib().branch_attn_fwd(_stream(stream), plan.handle, int(mode), ctypes.byref(io),
                                  _ptr(workspace), workspace.numel() * workspace.element_size()))
+
+
+def branch_attn_fwd_noalloc(plan: Plan, mode: int, q_main, q_br, k_br, v_br, k_step, v_step, o_main, o_br,
+                            lse_main, lse_br, stream=None):
+    """branch_attn_fwd with the library's static per-GPU scratch instead of a workspace."""
+    ks, vs = _ptr_array(k_step), _ptr_array(v_step)
+    io = BaFwdIO(_ptr(q_main), _ptr(q_br), _ptr(k_br), _ptr(v_br), ks, vs, _ptr(o_main), _ptr(o_br),
+                 _ptr(lse_main), _ptr(lse_br), None, None)
+    _check(lib().branch_attn_fwd_noalloc(_stream(stream), plan.handle, int(mode), ctypes.byref(io)))
 
 
 def branch_attn_bwd(plan: Plan, mode: int, q_main, q_br, k_br, v_br, k_step, v_step, o_main, o_br,

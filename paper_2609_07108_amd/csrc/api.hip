@@ -1,5 +1,6 @@
 // C ABI device entry points: validation, upload of the plan tables into the
 // caller's workspace, and the launch sequence of one forward / backward call.
+#include <mutex>
 #include <string>
 
 #include "ba_internal.h"
@@ -200,6 +201,64 @@ extern "C" int branch_attn_fwd(void* stream_, const ba_plan* plan, int32_t mode,
   if ((e = record(io->ring_end, stream)) != hipSuccess) return hip_fail(e, "event record");
   if ((e = launch_fwd_finalize(p, stream)) != hipSuccess) return hip_fail(e, "branch/merge launch");
   return BA_OK;
+}
+
+// ------------------------------------------------ forward without allocation
+// A file-scope device array stands in for the caller's workspace.  In host
+// code its name is only a stand-in for the device object: the address the
+// kernels may use is obtained per device with hipGetSymbolAddress, once, with
+// that device current, and kept here.
+namespace ba {
+namespace {
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;
+constexpr int kMaxDevices = 64;
+}  // namespace
+}  // namespace ba
+
+static __device__ __align__(256) char scratch[ba::kNoAllocScratchBytes];
+
+namespace ba {
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// address of this device's copy of `scratch` (looked up on first use)
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(BA_E_UNSUPPORTED, "device index beyond 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!ptr || ((uintptr_t)ptr & 255) != 0) return fail(BA_E_HIP, "scratch address is NULL or misaligned");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return BA_OK;
+}
+}  // namespace
+}  // namespace ba
+
+extern "C" int branch_attn_fwd_noalloc(void* stream, const ba_plan* plan, int32_t mode, const ba_fwd_io* io) {
+  if (!plan) return fail(BA_E_INVAL, "plan is NULL");
+  if (mode != BA_MODE_PER_STEP && mode != BA_MODE_FUSED && mode != BA_MODE_AUTO)
+    return fail(BA_E_INVAL, "unknown mode");
+  const Plan& P = plan->p;
+  mode = resolve_mode(P, mode);
+  if (P.cp_size > kMaxCp) return fail(BA_E_UNSUPPORTED, "cp_size > 32 unsupported");
+  const size_t need = workspace_layout(P, mode).fwd_total;
+  if (need > kNoAllocScratchBytes)
+    return fail(BA_E_WORKSPACE, "branch_attn_fwd_noalloc: this plan and mode need " + std::to_string(need) +
+                                    " bytes of scratch, the static scratch holds " +
+                                    std::to_string(kNoAllocScratchBytes) +
+                                    " (use BA_MODE_FUSED without rotary embedding, or branch_attn_fwd)");
+  void* ws = nullptr;
+  int rc = scratch_address(&ws);
+  if (rc) return rc;
+  return branch_attn_fwd(stream, plan, mode, io, ws, kNoAllocScratchBytes);
 }
 
 extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode, const ba_bwd_io* io,
