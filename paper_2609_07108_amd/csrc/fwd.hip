@@ -49,11 +49,17 @@ namespace {
 constexpr float kRescaleSlack = 8.f;  // log2 of the largest probability before a rescale
 constexpr int kFragAhead = 2;         // LDS operand fragments read ahead of their MFMAs
 constexpr int kKvBufs = 3;
+constexpr int kFwdRowBlocks = 1;  // 32-row blocks per wavefront (fwd_kernel's RB)
 
 }  // namespace
 
-template <int MODE>
-__global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
+// RB: 32-row blocks per wavefront.  RB = 2: four wavefronts (one per SIMD)
+// of 64 rows, every K/V fragment read feeding two MFMAs; RB = 1: eight
+// wavefronts (two per SIMD) of 32 rows, so that one wavefront's softmax runs
+// while the other's MFMAs do (a single wavefront leaves the matrix unit idle
+// between its MFMAs), at twice the LDS operand traffic per MFMA.
+template <int MODE, int RB>
+__global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
   // [buffer][K, V] plane tiles of 64 keys (see tile_off)
   __shared__ __attribute__((aligned(16))) bf16 kvbuf[kKvBufs][2][kFwdKeys * kHeadDim];
 
@@ -73,20 +79,20 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
   const int64_t kv_row_stride = (int64_t)p.hkv * kHeadDim;
 
   // ---- the lane's two rows (row block rb: row 64 w + 32 rb + qi)
-  int head[2];
-  bool valid[2];
-  TokInfo tk[2];
+  int head[RB];
+  bool valid[RB];
+  TokInfo tk[RB];
   // B operand of S^T = K Q^T (Q^T: k = head dims, n = rows), resident in the
   // accumulation registers; rows without a token load a row of the tile's
   // last token (finite, and their results are never written)
   // (the token records of both row blocks are read before any Q load is
   // issued: a compiler-visible load after the untracked Q loads would wait
   // for them too)
-  bf16x8 qreg[2][8];
-  const bf16* qptr[2];
+  bf16x8 qreg[RB][8];
+  const bf16* qptr[RB];
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb) {
-    const int row = 64 * wave + 32 * rb + qi;
+  for (int rb = 0; rb < RB; ++rb) {
+    const int row = 32 * RB * wave + 32 * rb + qi;
     const int tl = row / p.G;
     head[rb] = tile.kvh * p.G + (row - tl * p.G);
     valid[rb] = tl < tile.ntok;
@@ -97,16 +103,21 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
                             : p.q_br + ((int64_t)(-tq.qrow - 1) * p.hq + hq_row) * kHeadDim;
   }
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int c = 0; c < 8; ++c) load16_agpr(qreg[rb][c], qptr[rb] + 16 * c + 8 * half);
   __builtin_amdgcn_s_waitcnt(0);
 
-  f32x16 o[2][4];  // O^T accumulators, d = 32 dt + 8 (v/4) + 4 half + v%4
-  float m_use[2] = {-INFINITY, -INFINITY};  // reference maximum of the exponentials (log2)
-  float lsum[2] = {0.f, 0.f};               // this lane's share of the row sum
+  f32x16 o[RB][4];  // O^T accumulators, d = 32 dt + 8 (v/4) + 4 half + v%4
+  float m_use[RB];  // reference maximum of the exponentials (log2)
+  float lsum[RB];   // this lane's share of the row sum
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < RB; ++rb) {
+    m_use[rb] = -INFINITY;
+    lsum[rb] = 0.f;
+  }
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(o[rb][dt]);
 
@@ -169,14 +180,14 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     // column part, both lane constants precomputed once
     uint32_t frow[4], fcol[4];
 #pragma unroll
-    for (int m4 = 0; m4 < 4; ++m4) {
-      const int m = 4 * wave + m4;
+    for (int m4 = 0; m4 < 2 * RB; ++m4) {
+      const int m = 2 * RB * wave + m4;
       frow[m4] = (uint32_t)(dma_row<kFwdKeys>(m, lane) * (int)kv_row_stride) * 2u;
       fcol[m4] = (uint32_t)dma_col<kFwdKeys>(m, lane) * 2u;
     }
     auto fetch_piece = [&](const DmaTile& d, int k) {
       const int m4 = k >> 1, tensor = k & 1;
-      const int m = 4 * wave + m4;
+      const int m = 2 * RB * wave + m4;
       const uint32_t lim = (uint32_t)((d.nrow - 1) * (int)kv_row_stride) * 2u;  // wavefront-uniform
       const uint32_t off = min(frow[m4], lim) + fcol[m4];
       dma16_async(tensor ? d.vb : d.kb, off, d.dst + (uint32_t)tensor * kTileBytes + dma_dst_bytes<kFwdKeys>(m));
@@ -184,7 +195,7 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     auto fetch = [&](const KvCursor& c, int buf) {
       const DmaTile d = dma_tile(c, buf);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) fetch_piece(d, k);
+      for (int k = 0; k < 4 * RB; ++k) fetch_piece(d, k);
     };
 
     // ---- S^T of a tile: fragment f = 8 kb + c (keys 32 kb.., dims 16 c..)
@@ -192,7 +203,7 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     auto s_frag = [&](const bf16* ks, int f) -> bf16x8 {
       return ld16(&ks[tile_off<kFwdKeys>(32 * (f >> 3) + qi, 16 * (f & 7) + 8 * half)]);
     };
-    auto s_mfma = [&](f32x16 (&S)[2][2], int f, int rb, const bf16x8& a) {
+    auto s_mfma = [&](f32x16 (&S)[RB][2], int f, int rb, const bf16x8& a) {
       const int kb = f >> 3, c = f & 7;
       if (c == 0) mfma32_v_first(S[rb][kb], a, qreg[rb][c]);
       else mfma32_v(S[rb][kb], a, qreg[rb][c]);
@@ -206,9 +217,9 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     };
 
     // row maximum of S^T (raw scores) over the 64 keys of a tile
-    auto tile_max = [&](const f32x16 (&S)[2][2], float (&mx)[2]) {
+    auto tile_max = [&](const f32x16 (&S)[RB][2], float (&mx)[RB]) {
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
+      for (int rb = 0; rb < RB; ++rb) {
         float a = -INFINITY;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -225,18 +236,18 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     // j >= 32 -> V^T fragment (j-32)/2, row block j%2.  Softmax element e
     // (t4 = e/16, row block (e/8)%2, accumulator slot 8 (t4%2) + e%8 of key
     // block t4/2) in slot 52e/64, ahead of the MFMAs of key block t4.
-    auto iterate = [&](f32x16 (&Sc)[2][2], f32x16 (&Sn)[2][2], const bf16* ks_n, const bf16* vs_c,
-                       const float (&m_eff)[2], float (&mx_n)[2], auto&& issue_piece) {
+    auto iterate = [&](f32x16 (&Sc)[RB][2], f32x16 (&Sn)[RB][2], const bf16* ks_n, const bf16* vs_c,
+                       const float (&m_eff)[RB], float (&mx_n)[RB], auto&& issue_piece) {
       typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
       bf16x8 fq[kFragAhead + 1];
       typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
       // packed P^T as bf16 pairs, converted in the element's own slot:
       // [row block][t4] -> the B operand of the t4-th O^T MFMA
-      u32x4 pk[2][4];
-      float pv[2][4][8];
+      u32x4 pk[RB][4];
+      float pv[RB][4][8];
       auto frag = [&](int f) -> bf16x8 { return f < 16 ? s_frag(ks_n, f) : v_frag(vs_c, f - 16); };
       auto element = [&](int e) {
-        const int t4 = e >> 4, rb = (e >> 3) & 1, i = e & 7;
+        const int t4 = e / (8 * RB), rb = (e >> 3) % RB, i = e & 7;
         const float x = Sc[rb][t4 >> 1][8 * (t4 & 1) + i];
         const float pr = fast_exp2(__builtin_fmaf(x, p.scale_log2, -m_eff[rb]));
         pv[rb][t4][i] = pr;
@@ -247,30 +258,30 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
         return __builtin_bit_cast(bf16x8, pk[rb][t4]);
       };
       static_for<kFragAhead>([&](auto fc) { fq[fc.value] = frag(fc.value); });
-      static_for<64>([&](auto jc) {
+      static_for<32 * RB>([&](auto jc) {
         constexpr int j = decltype(jc)::value;
-        constexpr int f = j >> 1, rb = j & 1;
+        constexpr int f = j / RB, rb = j % RB;
         if constexpr (rb == 0 && f + kFragAhead < 32) fq[(f + kFragAhead) % (kFragAhead + 1)] = frag(f + kFragAhead);
-        static_for<64>([&](auto ec) {
+        static_for<32 * RB>([&](auto ec) {
           constexpr int e = decltype(ec)::value;
-          if constexpr ((e * 52) / 64 == j) element(e);
+          if constexpr ((e * 26) / 32 == j) element(e);
         });
-        if constexpr (j < 32) {
+        if constexpr (j < 16 * RB) {
           s_mfma(Sn, f, rb, fq[f % (kFragAhead + 1)]);
         } else {
           constexpr int g = f - 16, t4 = g >> 2, dt = g & 3;
           mfma32_acc<false>(o[rb][dt], fq[f % (kFragAhead + 1)], pa(rb, t4));  // P^T packed >= 5 slots ago
         }
-        if constexpr (j == 63) tile_max(Sn, mx_n);
+        if constexpr (j == 32 * RB - 1) tile_max(Sn, mx_n);
         if constexpr ((j & 7) == 4) issue_piece(j >> 3);  // direct loads of tile t+2, spread out
         __builtin_amdgcn_sched_barrier(0);
       });
     };
 
     // ---- apply the causal mask to the scores of a tile that needs it
-    auto mask_tile = [&](f32x16 (&S)[2][2], const KvCursor& c, float (&mx)[2]) {
+    auto mask_tile = [&](f32x16 (&S)[RB][2], const KvCursor& c, float (&mx)[RB]) {
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
+      for (int rb = 0; rb < RB; ++rb) {
         const int lim = valid[rb] ? visible_keys(tk[rb].P, c.j, p.C, seq.c) : 0;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -284,18 +295,20 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     };
     // ---- new reference maxima; rescale O and the sums of rows whose
     // maximum moved past the slack (rare after the first tiles)
-    auto update_max = [&](const float (&mx)[2], float (&m_eff)[2]) {
-      float m_new[2];
-      bool move[2];
+    auto update_max = [&](const float (&mx)[RB], float (&m_eff)[RB]) {
+      float m_new[RB];
+      bool move[RB];
+      bool any = false;
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
+      for (int rb = 0; rb < RB; ++rb) {
         m_new[rb] = mx[rb] * p.scale_log2;  // the scale is positive
         move[rb] = m_new[rb] > m_use[rb] + kRescaleSlack || (m_use[rb] == -INFINITY && m_new[rb] > -INFINITY);
+        any = any || move[rb];
       }
-      if (__ballot(move[0] || move[1])) {
+      if (__ballot(any)) {
         mfma_drain();  // pending O^T updates complete before the vector ALUs touch O
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
+        for (int rb = 0; rb < RB; ++rb) {
           const float alpha = move[rb] ? fast_exp2(m_use[rb] - m_new[rb]) : 1.f;  // m_use = -inf gives 0
           if (move[rb]) m_use[rb] = m_new[rb];
           lsum[rb] *= alpha;
@@ -305,7 +318,7 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
         mfma_drain();
       }
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) m_eff[rb] = m_use[rb] == -INFINITY ? 0.f : m_use[rb];
+      for (int rb = 0; rb < RB; ++rb) m_eff[rb] = m_use[rb] == -INFINITY ? 0.f : m_use[rb];
     };
 
     KvCursor cur = seek(p.step_first);
@@ -315,22 +328,22 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
       if (nxt.i < step_end) fetch(nxt, 1);
       __builtin_amdgcn_s_waitcnt(0);
       lds_barrier();
-      f32x16 Sa[2][2], Sb[2][2];
-      float mx[2], m_eff[2];
+      f32x16 Sa[RB][2], Sb[RB][2];
+      float mx[RB], m_eff[RB];
       // prologue: S^T of the first tile
-      static_for<32>([&](auto jc) {
+      static_for<16 * RB>([&](auto jc) {
         constexpr int j = decltype(jc)::value;
-        s_mfma(Sa, j >> 1, j & 1, s_frag(&kvbuf[0][0][0], j >> 1));
+        s_mfma(Sa, j / RB, j % RB, s_frag(&kvbuf[0][0][0], j / RB));
       });
       mfma_drain();  // the scores are read by the vector ALUs next
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) vacc_settle(Sa[rb][kb]);
       tile_max(Sa, mx);
       int t = 0;
       // tile t is in buffer t % 3; scores of tile t in Sa (t even) or Sb
-      auto step = [&](f32x16 (&Sc)[2][2], f32x16 (&Sn)[2][2]) {
+      auto step = [&](f32x16 (&Sc)[RB][2], f32x16 (&Sn)[RB][2]) {
         const KvCursor n2 = next(nxt);
         // with no tile t+2 the loads repeat tile t into the idle buffer
         const KvCursor ld = n2.i < step_end ? n2 : cur;
@@ -356,18 +369,18 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
     }
   }
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) acc_settle(o[rb][dt]);
 
   // ------------------------------------------------------------ epilogues
-  // per row block; every lane runs both so cross-lane exchanges stay uniform
-  float l_tot[2];
+  // per row block; every lane runs all of them so cross-lane exchanges stay uniform
+  float l_tot[RB];
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb) l_tot[rb] = lsum[rb] + xor32(lsum[rb]);
+  for (int rb = 0; rb < RB; ++rb) l_tot[rb] = lsum[rb] + xor32(lsum[rb]);
 
   auto finish = [&](int rb) {
-    const int64_t acc_row = (int64_t)(tile.tok_begin + (64 * wave + 32 * rb + qi) / p.G) * p.hq + head[rb];
+    const int64_t acc_row = (int64_t)(tile.tok_begin + (32 * RB * wave + 32 * rb + qi) / p.G) * p.hq + head[rb];
     f32x16 st_o[4];
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) st_o[dt] = o[rb][dt];
@@ -516,8 +529,8 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdParams p) {
       }
     if (half == 0) *lse_out = lse2 * kLn2;
   };
-  finish(0);
-  finish(1);
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) finish(rb);
 }
 
 // ------------------------------------------------------------ finalize
@@ -632,8 +645,9 @@ hipError_t launch_fwd_finalize(const FwdParams& p, hipStream_t stream) {
 hipError_t launch_fwd(const FwdParams& p, int mode, hipStream_t stream) {
   if (p.num_tiles == 0) return hipSuccess;
   dim3 grid(p.num_tiles), block(256);
-  if (mode == kModeStep) hipLaunchKernelGGL(fwd_kernel<kModeStep>, grid, block, 0, stream, p);
-  else hipLaunchKernelGGL(fwd_kernel<kModeFused>, grid, block, 0, stream, p);
+  block = dim3(512 / kFwdRowBlocks);
+  if (mode == kModeStep) hipLaunchKernelGGL((fwd_kernel<kModeStep, kFwdRowBlocks>), grid, block, 0, stream, p);
+  else hipLaunchKernelGGL((fwd_kernel<kModeFused, kFwdRowBlocks>), grid, block, 0, stream, p);
   return hipGetLastError();
 }
 
