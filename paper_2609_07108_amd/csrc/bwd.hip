@@ -121,11 +121,11 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
 // Workgroup of 4 wavefronts (one per SIMD, up to 512 registers each) on 128
 // keys, as two wavefront pairs of 64 keys: pair p owns keys 64p..64p+63.
 // Inside a pair the work of the four contractions is split by operand:
-//   score wavefront (w = p):     K scale log2e of the pair's keys in
-//                                registers; S' = Q (K scale log2e)^T - LSE
-//                                log2e (the accumulation starts from -LSE
-//                                log2e), P = exp2(S') with the causal mask,
-//                                P handed to the partner through LDS,
+//   score wavefront (w = p):     K of the pair's keys in registers;
+//                                S = Q K^T, P = exp2(S scale log2e - LSE
+//                                log2e) with the causal mask (one fused
+//                                multiply-add and one exp2 per element), P
+//                                handed to the partner through LDS,
 //                                dV += P^T dO
 //   gradient wavefront (w = 2+p): V in registers; dP - Delta = dO V^T -
 //                                Delta (the accumulation starts from
@@ -315,20 +315,18 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   const bf16* kvsrc = (scorer ? p.k_step[tile.step] : p.v_step[tile.step]) + tile.kvh * kHeadDim;
 
   if (scorer) {
-    // K scale log2e of the lane's keys (B operands of S'), resident in the
-    // accumulation registers.  Rounding the scaled K to bf16 perturbs each
-    // score by about 2^-9 of |q| |k| scale (relative), well inside the
-    // gradients' tolerance, and saves one multiply-add per probability.
+    // K of the lane's keys (B operands of S), resident in the accumulation
+    // registers.  The softmax scale is applied in fp32 per score: folding it
+    // into a bf16 copy of K perturbs every score by about 2^-9 of its
+    // magnitude, which grows with the logits (dK, dV relative error 3e-2 at
+    // score standard deviation 16 against 3e-3 at 1).
     bf16x8 kreg[2][8];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
         const bf16x8 kr = ld16(kvsrc + (key0 + kload[kb]) * kv_row_stride + 16 * c + 8 * half);
-        bf16x8 ks;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) ks[e] = (bf16)((float)kr[e] * p.scale_log2);
-        asm volatile("" : "=a"(kreg[kb][c]) : "0"(ks));
+        asm volatile("" : "=a"(kreg[kb][c]) : "0"(kr));
       }
     zero_acc();
     __builtin_amdgcn_s_waitcnt(0);
@@ -375,7 +373,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
       // v = 4q + e%4 (row 32 rb + 8q + 4h + e%4)
       auto element = [&](int e) {
         const int rb = e >> 5, q = (e >> 3) & 3, kb = (e >> 2) & 1, c = e & 3, v = 4 * q + c;
-        float pr = fast_exp2(s[rb][kb][v]);
+        float pr = fast_exp2(__builtin_fmaf(s[rb][kb][v], p.scale_log2, nl[rb][v]));
         if (MASK) {
           const int lim = c == 0 ? sp[rb][q].x : c == 1 ? sp[rb][q].y : c == 2 ? sp[rb][q].z : sp[rb][q].w;
           pr = kpos[kb] <= lim ? pr : 0.f;
@@ -386,7 +384,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
       auto mfma = [&](int j, const bf16x8& a) {
         if (j < 32) {
           const int rb = j >> 4, c = (j >> 1) & 7, kb = j & 1;
-          if (c == 0) mfma32_v_init(s[rb][kb], a, kreg[kb][0], nl[rb]);
+          if (c == 0) mfma32_v_first(s[rb][kb], a, kreg[kb][0]);
           else mfma32_v(s[rb][kb], a, kreg[kb][c]);
         } else {
           const int jj = j - 32, t = jj >> 3, nt = (jj >> 1) & 3, kb = jj & 1;
