@@ -742,12 +742,13 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
     // ---- cursor over (ring step, 64-key tile), as in the forward
     const int step_end = p.step_first + p.step_count;
     auto seek = [&](int i) {
-      KvCursor c{i, 0, 0, 0};
+      KvCursor c{i, 0, 0, 0, 0};
       for (; c.i < step_end; ++c.i) {
         c.j = ((p.rank - c.i) % p.C + p.C) % p.C;
         c.lim_hi = visible_keys(Pmax, c.j, p.C, seq.c);
         if (c.lim_hi > 0) break;
       }
+      c.lim_lo = visible_keys(Pmin, c.j, p.C, seq.c);
       return c;
     };
     auto next = [&](KvCursor c) {
@@ -768,17 +769,20 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
     };
     // the ring block's K/V bases, re-read from the kernel arguments only
     // when the walk moves to another block
+    // (their sequence segment and KV head already applied: a tile adds only
+    // kv0 rows)
     int cj = -1;
     const bf16* ckb = nullptr;
     const bf16* cvb = nullptr;
     auto dma_tile = [&](const KvCursor& c, int buf) {
       if (c.j != cj) {
         cj = c.j;
-        ckb = p.k_step[cj];
-        cvb = p.v_step[cj];
+        const int64_t seg = (int64_t)seq.seg_off * kv_row_stride + tile.kvh * kHeadDim;
+        ckb = p.k_step[cj] + seg;
+        cvb = p.v_step[cj] + seg;
         asm volatile("" : "+s"(ckb), "+s"(cvb));
       }
-      const int64_t row0 = ((int64_t)seq.seg_off + c.kv0) * kv_row_stride + tile.kvh * kHeadDim;
+      const int64_t row0 = (int64_t)c.kv0 * kv_row_stride;
       DmaTile d{uniform_ptr(ckb + row0), uniform_ptr(cvb + row0), kv_lds + (uint32_t)(2 * buf) * kTileBytes,
                 c.lim_hi - c.kv0};
       asm volatile("" : "+s"(d.kb), "+s"(d.vb));
@@ -948,7 +952,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
         const KvCursor nx = next(cur);
         const bool more = nx.i < step_end;
         const DmaTile dn = dma_tile(more ? nx : cur, (t + 1) % kDqBufs);
-        const bool mask = cur.kv0 + kFwdKeys > visible_keys(Pmin, cur.j, p.C, seq.c);
+        const bool mask = cur.kv0 + kFwdKeys > cur.lim_lo;
         // the first tile's stand-in previous tile reads this tile's (finite) K
         iterate(std::false_type{}, t % kDqBufs, t == 0 ? 0 : (t - 1) % kDqBufs, cur, mask, dn, more);
         wait_vmcnt_lgkm0<0>();  // tile t+1 has landed for this wavefront

@@ -130,12 +130,13 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
     // tile's largest causal limit can see
     const int step_end = p.step_first + p.step_count;
     auto seek = [&](int i) {
-      KvCursor c{i, 0, 0, 0};
+      KvCursor c{i, 0, 0, 0, 0};
       for (; c.i < step_end; ++c.i) {
         c.j = ((p.rank - c.i) % p.C + p.C) % p.C;
         c.lim_hi = visible_keys(Pmax, c.j, p.C, seq.c);
         if (c.lim_hi > 0) break;
       }
+      c.lim_lo = visible_keys(Pmin, c.j, p.C, seq.c);
       return c;
     };
     auto next = [&](KvCursor c) {
@@ -159,17 +160,20 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
     };
     // the ring block's K/V bases, re-read from the kernel arguments only
     // when the walk moves to another block
+    // (their sequence segment and KV head already applied: a tile adds only
+    // kv0 rows)
     int cj = -1;
     const bf16* ckb = nullptr;
     const bf16* cvb = nullptr;
     auto dma_tile = [&](const KvCursor& c, int buf) {
       if (c.j != cj) {
         cj = c.j;
-        ckb = p.k_step[cj];
-        cvb = p.v_step[cj];
+        const int64_t seg = (int64_t)seq.seg_off * kv_row_stride + tile.kvh * kHeadDim;
+        ckb = p.k_step[cj] + seg;
+        cvb = p.v_step[cj] + seg;
         asm volatile("" : "+s"(ckb), "+s"(cvb));
       }
-      const int64_t row0 = ((int64_t)seq.seg_off + c.kv0) * kv_row_stride + tile.kvh * kHeadDim;
+      const int64_t row0 = (int64_t)c.kv0 * kv_row_stride;
       DmaTile d{uniform_ptr(ckb + row0), uniform_ptr(cvb + row0), kv_lds + (uint32_t)(2 * buf) * kTileBytes,
                 c.lim_hi - c.kv0};
       asm volatile("" : "+s"(d.kb), "+s"(d.vb));
@@ -216,7 +220,9 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
       return ld_tr8<kFwdKeys>(vs, 32 * dt, 16 * t4 + 4 * half, 16 * t4 + 8 + 4 * half, lane);
     };
 
-    // row maximum of S^T (raw scores) over the 64 keys of a tile
+    // maximum of S^T (raw scores) over this lane's 32 keys of a tile (the
+    // other 32 keys of the row are in lane l ^ 32); the two halves are only
+    // combined when the row's reference maximum may have to move
     auto tile_max = [&](const f32x16 (&S)[RB][2], float (&mx)[RB]) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
@@ -225,7 +231,7 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int v = 0; v < 16; ++v) a = fmaxf(a, S[rb][kb][v]);
-        mx[rb] = fmaxf(a, xor32(a));
+        mx[rb] = a;
       }
     };
 
@@ -295,6 +301,8 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
     };
     // ---- new reference maxima; rescale O and the sums of rows whose
     // maximum moved past the slack (rare after the first tiles)
+    // (mx holds half-row maxima: a row moves iff either half asks to, and
+    // both halves of the row then take the same, exchanged, maximum)
     auto update_max = [&](const float (&mx)[RB], float (&m_eff)[RB]) {
       float m_new[RB];
       bool move[RB];
@@ -302,10 +310,14 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         m_new[rb] = mx[rb] * p.scale_log2;  // the scale is positive
-        move[rb] = m_new[rb] > m_use[rb] + kRescaleSlack || (m_use[rb] == -INFINITY && m_new[rb] > -INFINITY);
-        any = any || move[rb];
+        any = any || m_new[rb] > m_use[rb] + kRescaleSlack || (m_use[rb] == -INFINITY && m_new[rb] > -INFINITY);
       }
       if (__ballot(any)) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          m_new[rb] = fmaxf(mx[rb], xor32(mx[rb])) * p.scale_log2;
+          move[rb] = m_new[rb] > m_use[rb] + kRescaleSlack || (m_use[rb] == -INFINITY && m_new[rb] > -INFINITY);
+        }
         mfma_drain();  // pending O^T updates complete before the vector ALUs touch O
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
@@ -348,7 +360,7 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
         // with no tile t+2 the loads repeat tile t into the idle buffer
         const KvCursor ld = n2.i < step_end ? n2 : cur;
         const DmaTile d2 = dma_tile(ld, (t + 2) % kKvBufs);
-        if (cur.kv0 + kFwdKeys > visible_keys(Pmin, cur.j, p.C, seq.c)) mask_tile(Sc, cur, mx);
+        if (cur.kv0 + kFwdKeys > cur.lim_lo) mask_tile(Sc, cur, mx);
         update_max(mx, m_eff);
         // with no tile t+1 the S^T MFMAs read a stale buffer and are discarded
         iterate(Sc, Sn, &kvbuf[(t + 1) % kKvBufs][0][0], &kvbuf[t % kKvBufs][1][0], m_eff, mx,

@@ -86,6 +86,7 @@ struct BwdParams {
 // kv0 of a 64-key tile, keys of the block visible to the tile lim_hi).
 struct KvCursor {
   int i, j, kv0, lim_hi;
+  int lim_lo;  // keys of block j every row of the query tile sees (tiles below need no mask)
 };
 
 hipError_t launch_fwd(const FwdParams& p, int mode, hipStream_t stream);
