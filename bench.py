@@ -37,9 +37,9 @@ PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/c
 # calibration (profiles/traffic_eagle3-K3-L262144-cp8r0.md).  A figure only
 # applies while the kernel's source is the one that was measured.
 MEASURED_TRAFFIC = {
-    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "adfb73f9aba2e11a", "bytes": 50527610471},
-    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "adfb73f9aba2e11a", "bytes": 7945711183},
-    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "c35f5b38d7409106", "bytes": 7145979429},
+    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "d0d63ec323720f5f", "bytes": 50306357928},
+    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "d0d63ec323720f5f", "bytes": 12011849103},
+    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "51b434b871aa004e", "bytes": 9075458882},
 }
 
 def measured_traffic(kernel: str, workload: str, mode: str):
