@@ -1024,14 +1024,19 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
       const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
       float sdot = 0.f, pdot = 0.f;
       if (active) {
+        // the row's Q and dO are re-read (L2-resident) rather than kept in
+        // the accumulation registers past the key walk, which would make the
+        // compiler spill them around it
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
           const bf16x8 kv = ld16(kb + 16 * c + 8 * half);
           const bf16x8 vv = ld16(vb + 16 * c + 8 * half);
+          const bf16x8 qv = ld16(qp[rb] + 16 * c + 8 * half);
+          const bf16x8 gv = ld16(gp[rb] + 16 * c + 8 * half);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            sdot += (float)qreg[rb][c][e] * (float)kv[e];
-            pdot += (float)greg[rb][c][e] * (float)vv[e];
+            sdot += (float)qv[e] * (float)kv[e];
+            pdot += (float)gv[e] * (float)vv[e];
           }
         }
       }

@@ -483,11 +483,15 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
       const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
       float dot = 0.f;
       if (active) {
+        // the row's Q is re-read (L2-resident) rather than kept in the
+        // accumulation registers past the key walk, which would make the
+        // compiler spill them around it
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
           const bf16x8 kv = ld16(kb + 16 * c + 8 * half);
+          const bf16x8 qv = ld16(qptr[rb] + 16 * c + 8 * half);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) dot += (float)qreg[rb][c][e] * (float)kv[e];
+          for (int e = 0; e < 8; ++e) dot += (float)qv[e] * (float)kv[e];
         }
       }
       dot += xor32(dot);
