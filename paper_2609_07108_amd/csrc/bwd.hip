@@ -20,8 +20,10 @@
 //   dq         : dQ, query-tile parallel like the forward (256-row tiles,
 //                64 rows per wavefront): per key tile S^T = K Q^T,
 //                dP^T = V dO^T, dS^T, dQ^T += K^T dS^T, software-pipelined
-//                across key tiles, with the branch-local keys handled in the
-//                epilogue.  Splitting dQ off
+//                across key tiles; the branch-local keys' terms are the
+//                accumulators' start value in the fused schedule and are
+//                added by the finalize kernel in the per-step one.
+//                Splitting dQ off
 //                costs two extra contractions but avoids fp32 atomics, whose
 //                throughput (about one 4-byte update per L2 channel and clock)
 //                would otherwise bound the whole backward.
@@ -730,13 +732,77 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
   __builtin_amdgcn_s_waitcnt(0);
 
   f32x16 dq[2][4];
+  if constexpr (MODE == kModeStep) {
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+    for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(dq[rb][dt]);
+      for (int dt = 0; dt < 4; ++dt) mfma32_acc_zero(dq[rb][dt]);
+  }
 
   const int Pmin = p.toks[tile.tok_begin].P;
   const int Pmax = p.toks[tile.tok_begin + tile.ntok - 1].P;
+
+  // ---- FUSED: the dQ accumulators of a branch row start at its
+  // branch-local terms, the sum over its branch keys (chain members 0..i,
+  // or the whole block; at most BA_MAX_GROUP_LEN, on the vector ALUs) of
+  // dS K with P and dS from the row statistics as for a main key.  The
+  // scores take the register-held Q and dO (dims 16 c + 8 half + 0..7) and
+  // K, V read in that layout; dS K takes K again in the accumulator layout
+  // (dims 32 dt + 8 vq + 4 half + 0..3), all of a key in one round trip to
+  // memory.  A lane past its keys (or without any) reloads a valid row and
+  // gives it weight 0.
+  auto seed_branch = [&](int rb) {
+    int nb = 0;
+    GroupInfo gi{0, 1, 0, 0, 0, 0, {0, 0}};
+    if (valid[rb] && tk[rb].grp >= 0) {
+      gi = p.groups[tk[rb].grp];
+      nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk[rb].gidx + 1 : gi.len;
+    }
+    f32x16 acc[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x16{};
+    if (__ballot(nb > 0)) {
+      for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
+        if (__ballot(b < nb) == 0) break;
+        const int bu = min(b, max(nb - 1, 0));
+        const int64_t krow = (int64_t)gi.row0 + (int64_t)bu * gi.stride;
+        const bf16* kb = p.k_br + krow * kv_row_stride + tile.kvh * kHeadDim;
+        const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
+        bf16x8 kd[8], vd[8];
+        bf16x4 kk[4][4];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          kd[c] = ld16(kb + 16 * c + 8 * half);
+          vd[c] = ld16(vb + 16 * c + 8 * half);
+        }
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int vq = 0; vq < 4; ++vq)
+            kk[dt][vq] = *reinterpret_cast<const bf16x4*>(kb + 32 * dt + 8 * vq + 4 * half);
+        float sdot = 0.f, pdot = 0.f;
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            sdot += (float)qreg[rb][c][e] * (float)kd[c][e];
+            pdot += (float)greg[rb][c][e] * (float)vd[c][e];
+          }
+        sdot += xor32(sdot);
+        pdot += xor32(pdot);
+        const float pr = b < nb ? fast_exp2(sdot * p.scale_log2 + nl2[rb]) : 0.f;
+        const float ds = pr * (pdot + ndl[rb]);
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int vq = 0; vq < 4; ++vq)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) acc[dt][4 * vq + c] += ds * (float)kk[dt][vq][c];
+      }
+    }
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) asm volatile("" : "=a"(dq[rb][dt]) : "0"(acc[dt]));
+  };
 
   {
     // ---- cursor over (ring step, 64-key tile), as in the forward
@@ -931,11 +997,16 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
 
     KvCursor cur = seek(p.step_first);
     if (cur.i < step_end) {
-      {
-        const DmaTile d0 = dma_tile(cur, 0);
+      const DmaTile d0 = dma_tile(cur, 0);
 #pragma unroll
-        for (int k = 0; k < 8; ++k) fetch_piece(d0, k);
-      }
+      for (int k = 0; k < 8; ++k) fetch_piece(d0, k);
+    }
+    // FUSED: the branch-local terms while the first tile is in flight
+    if constexpr (MODE == kModeFused) {
+      seed_branch(0);
+      seed_branch(1);
+    }
+    if (cur.i < step_end) {
       // the stand-in previous tile: scores -inf, so its dS are zero
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb) {
@@ -1008,51 +1079,6 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
           *reinterpret_cast<float4*>(dst + 32 * dt + 8 * vq + 4 * half) = a;
         }
       return;
-    }
-    // ---- branch-local keys of this row (vector ALUs)
-    int nb = 0;
-    GroupInfo gi{0, 1, 0, 0, 0, 0, {0, 0}};
-    if (valid[rb] && tk[rb].grp >= 0) {
-      gi = p.groups[tk[rb].grp];
-      nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk[rb].gidx + 1 : gi.len;
-    }
-    for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
-      const bool active = b < nb;
-      if (__ballot(active) == 0) break;
-      const int64_t krow = (int64_t)gi.row0 + (int64_t)b * gi.stride;
-      const bf16* kb = p.k_br + krow * kv_row_stride + tile.kvh * kHeadDim;
-      const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
-      float sdot = 0.f, pdot = 0.f;
-      if (active) {
-        // the row's Q and dO are re-read (L2-resident) rather than kept in
-        // the accumulation registers past the key walk, which would make the
-        // compiler spill them around it
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          const bf16x8 kv = ld16(kb + 16 * c + 8 * half);
-          const bf16x8 vv = ld16(vb + 16 * c + 8 * half);
-          const bf16x8 qv = ld16(qp[rb] + 16 * c + 8 * half);
-          const bf16x8 gv = ld16(gp[rb] + 16 * c + 8 * half);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            sdot += (float)qv[e] * (float)kv[e];
-            pdot += (float)gv[e] * (float)vv[e];
-          }
-        }
-      }
-      sdot += xor32(sdot);
-      pdot += xor32(pdot);
-      if (!active) continue;
-      const float pr = fast_exp2(sdot * p.scale_log2 + nl2[rb]);
-      const float ds = pr * (pdot + ndl[rb]);
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int vq = 0; vq < 4; ++vq) {
-          const bf16x4 kk = *reinterpret_cast<const bf16x4*>(kb + 32 * dt + 8 * vq + 4 * half);
-#pragma unroll
-          for (int c = 0; c < 4; ++c) st[dt][4 * vq + c] += ds * (float)kk[c];
-        }
     }
     if (!valid[rb]) return;
 

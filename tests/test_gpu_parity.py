@@ -147,9 +147,15 @@ def test_per_step_and_fused_agree(cuda):
         RS.run_fwd(share, out, mode, RS.workspace(share, mode))
         outs.append(out)
     torch.cuda.synchronize()
+    # both schedules are fp32 inside and round O to bf16 once, so they may
+    # differ by one bf16 unit in the last place: 2^-7 relative at |O| >= 1,
+    # at most 2^-7 absolute below (the two merge the branch-local keys in a
+    # different order, so that rounding does happen)
     for k in ("o_main", "o_br"):
-        d = (outs[0][k].float() - outs[1][k].float()).abs().max().item()
-        assert d <= 2 * 2.0 ** -8, (k, d)
+        a, b = outs[0][k].float(), outs[1][k].float()
+        tol = 2.0 ** -7 * torch.maximum(a.abs(), b.abs()).clamp(min=1.0)
+        excess = ((a - b).abs() - tol).max().item()
+        assert excess <= 0, (k, excess)
     for k in ("lse_main", "lse_br"):
         d = (outs[0][k] - outs[1][k]).abs().max().item()
         assert d <= 1e-4, (k, d)
