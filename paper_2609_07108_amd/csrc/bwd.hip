@@ -986,8 +986,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
             constexpr int e = decltype(ec)::value;
             if constexpr (dq_slot0(e) == j) element(s0, p0, ds0, sv0, e);
           });
-          if constexpr ((j & 7) == 4 && j < 64) {
-            if (load_next) fetch_piece(dn, j >> 3);
+          // direct loads of tile t+1, in the first slots: its buffer (tile
+          // t-2's) is free from the iteration's start
+          if constexpr (j < 8) {
+            if (load_next) fetch_piece(dn, j);
           }
         }
         if constexpr (act) mfma(j, opq[f % (kDqAhead + 1)]);

@@ -279,7 +279,9 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
           mfma32_acc<false>(o[rb][dt], fq[f % (kFragAhead + 1)], pa(rb, t4));  // P^T packed >= 5 slots ago
         }
         if constexpr (j == 32 * RB - 1) tile_max(Sn, mx_n);
-        if constexpr ((j & 7) == 4) issue_piece(j >> 3);  // direct loads of tile t+2, spread out
+        // direct loads of tile t+2, in the first slots: its buffer (tile t-1's)
+        // is free from the iteration's start
+        if constexpr (j < 4 * RB) issue_piece(j);
         __builtin_amdgcn_sched_barrier(0);
       });
     };
