@@ -113,7 +113,8 @@ struct BwdTile {
   int32_t q_full;   // tokens >= q_full see all of them
   int32_t q_end;
   int32_t slot;     // -1: the item writes dK, dV; else its fp32 partial slot
-  int32_t pad[3];
+  int32_t walk_down;  // 1: query tiles from the last down, 0: from the first up
+  int32_t pad[2];
 };
 
 // Keys whose query range was split into several work items: the items'
@@ -133,6 +134,10 @@ struct KvSplit {
 // longest items split along the query range, so one launch still fills the
 // GPU (four items per compute unit of an MI355X).
 constexpr int32_t kKvSplitBelow = 1024;
+// dK/dV work items that start together on the GPU: one per compute unit
+// (MI355X: 256), one workgroup per compute unit.  Only the items' walk
+// direction depends on it (an L2 locality choice, no effect on results).
+constexpr int32_t kKvRoundItems = 256;
 // smallest piece of a split item, in 64-row query tiles
 constexpr int32_t kKvSplitMinTiles = 16;
 

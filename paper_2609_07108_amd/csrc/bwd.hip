@@ -140,7 +140,10 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
 // registers) sit in two register files.  No atomics.
 //
 // Query tiles (tokens x the G heads of the KV head, ordered by causal limit)
-// are walked in order.  In stage i the score wavefronts compute P of tile
+// are walked from the last down or from the first up, as the planner sets
+// per item (walk_down) so that items running at the same time read the
+// same Q and dO tiles at about the same time and share them in L2.  Below,
+// "tile i" of a stage is the one at stage position i.  In stage i the score wavefronts compute P of tile
 // i+1 and dV of tile i (P of tile i kept in registers from stage i-1); the
 // gradient wavefronts compute dK of tile i with P of tile i written by their
 // partner in stage i-1.  One barrier per stage publishes P and the direct
@@ -236,9 +239,9 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   const int stl = lane / G, shg = lane - stl * G;
   const uint32_t q_lds = lds_addr(&sm.qs[0]);
   const uint32_t g_lds = lds_addr(&sm.gs[0]);
-  // Q of tile kq (score wavefronts) or dO of tile kg (gradient wavefronts);
-  // past the last tile the last one again, into the tile's own (idle)
-  // buffer.  A stage's loads go out in 9 pieces spread over its schedule:
+  // Q of the tile at stage position kq (score wavefronts) or dO of the one
+  // at position kg (gradient wavefronts); past the last position its tile
+  // again, into the position's own (idle) buffer.  A stage's loads go out in 9 pieces spread over its schedule:
   // pieces 0-7 are the row loads (rows 32 pair + 16 (piece/4) + lane/4,
   // plane piece%4), piece 8 the statistic.
   const bf16* rows_src = scorer ? p.qtok : p.gtok;
@@ -247,10 +250,12 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
     int qt0, nt;
     uint32_t b;
   };
+  // the query tile at stage position k (see walk_down)
+  auto tile_at = [&](int k) { return tile.walk_down ? ntiles - 1 - k : k; };
   auto dma_begin = [&](int kq, int kg) __attribute__((always_inline)) {
     const int k = scorer ? kq : kg;
     DmaStage d;
-    d.qt0 = tile.q_begin + (k < ntiles ? k : ntiles - 1) * tpt;
+    d.qt0 = tile.q_begin + tile_at(k < ntiles ? k : ntiles - 1) * tpt;
     d.nt = tile.q_end - d.qt0;  // tokens left from qt0
     d.b = scorer ? q_lds + (uint32_t)(k % kQBufs) * (uint32_t)sizeof(QSide)
                  : g_lds + (uint32_t)(k % kGBufs) * (uint32_t)sizeof(GSide);
@@ -296,12 +301,15 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
 
   const LaneOffsets lo = lane_offsets(lane);
 
-  // Tiles [t_lo, t_hi) need no mask: every row has a token and sees all
-  // keys of the block (tokens from q_full on do).
+  // Tiles u_lo .. u_hi-1 need no mask: every row has a token and sees all
+  // keys of the block (tokens from q_full on do).  Stage positions [t_lo,
+  // t_hi) hold them.
   int t_lo = ntiles, t_hi = ntiles;
   if (tile.nk == kBwdKeys && tpt * G == kBwdRows) {
-    t_lo = min(ntiles, max(0, (tile.q_full - tile.q_begin + tpt - 1) / tpt));
-    t_hi = max(t_lo, (tile.q_end - tile.q_begin) / tpt);
+    const int u_lo = min(ntiles, max(0, (tile.q_full - tile.q_begin + tpt - 1) / tpt));
+    const int u_hi = max(u_lo, (tile.q_end - tile.q_begin) / tpt);
+    t_lo = tile.walk_down ? ntiles - u_hi : u_lo;
+    t_hi = tile.walk_down ? ntiles - u_lo : u_hi;
   }
 
   // Q of tiles 0 and 1, dO of tile 0

@@ -267,7 +267,7 @@ static int build_plan(const ba_problem* pr, Plan& P) {
         if (qb == si.tok_end) continue;
         for (int32_t h = 0; h < pr->hkv; ++h)
           bt.push_back(KeyedB{(int64_t)(si.tok_end - qb),
-                              BwdTile{j, s, h, u0, nk, qb, qf, si.tok_end, -1, {0, 0, 0}}});
+                              BwdTile{j, s, h, u0, nk, qb, qf, si.tok_end, -1, 0, {0, 0}}});
       }
     }
     if (!bt.empty()) min_items = std::min(min_items, (int32_t)bt.size());
@@ -303,6 +303,15 @@ static int build_plan(const ba_problem* pr, Plan& P) {
       bt.swap(split);
     }
     std::stable_sort(bt.begin(), bt.end(), [](const KeyedB& a, const KeyedB& b) { return a.work > b.work; });
+    // Walk directions for L2 sharing of the Q and dO tiles.  Every item's
+    // query range ends at its sequence's last token, and in this longest-
+    // first order the lengths of a round of kKvRoundItems items fall about
+    // linearly, so the items of an even round start together (those of
+    // round 0 at the launch, later ones as a whole previous pair of rounds
+    // ends) and walk from the last tile down in step, while an odd round's
+    // items start one after another, each as early as its range is long,
+    // and walking from their first tile up are in step too.
+    for (size_t n = 0; n < bt.size(); ++n) bt[n].t.walk_down = (n / kKvRoundItems) % 2 == 0 ? 1 : 0;
     for (auto& k : bt) P.bwd_tiles.push_back(k.t);
     P.bwd_step_off[i + 1] = (int32_t)P.bwd_tiles.size();
   }
