@@ -297,6 +297,197 @@ __global__ __launch_bounds__(256, 2) void proj_gemm_kernel(const ProjGemmParams 
   }
 }
 
+// ------------------------------------------------------------------ wide
+// The forward product (both operands k-major, K % kWBk == 0) on 256 x 256
+// output tiles: eight wavefronts (two per SIMD), wavefront w computing the
+// 128 x 64 block at rows 128 (w / 4), columns 64 (w % 4) as 4 x 2 MFMA
+// accumulators, so each k-step's six operand fragments (6 KB) feed eight
+// MFMAs (0.75 KB of LDS reads per MFMA against 1 KB for the 64 x 64 blocks
+// above).  Operands go global -> LDS by direct loads (no register staging,
+// no LDS store instructions) into kWStages stages of kWBk reduction values,
+// one barrier per stage.
+namespace {
+
+constexpr int kWTile = 256;                          // output tile rows and columns
+constexpr int kWBk = 64;                             // reduction values per stage
+constexpr int kWStages = 2;
+constexpr int kWChunks = kWBk / 8;                   // 16-byte chunks per operand row of a stage
+constexpr int kWKsteps = kWBk / 16;                  // MFMA k-steps per stage
+constexpr uint32_t kWOpBytes = kWTile * kWBk * 2;    // one operand of one stage
+constexpr int kWPieces = (int)(2 * kWOpBytes / 1024 / 8);  // 1 KB direct loads per wavefront and stage
+constexpr int kWRows = 128;                          // epilogue rows staged per pass
+constexpr int kWStageLd = kWTile + 8;                // fp32 staging pitch
+constexpr int kWSmem = (int)(kWStages * 2 * kWOpBytes) > kWRows * kWStageLd * 4 ? (int)(kWStages * 2 * kWOpBytes)
+                                                                                 : kWRows * kWStageLd * 4;
+
+// operand tile of a stage: 256 rows x kWBk reduction values (2 kWBk bytes
+// per row); 16-byte chunk c of row r sits at chunk c ^ ((r / (16 / kWChunks))
+// % kWChunks), so each group of 16 lanes of a fragment read (16 consecutive
+// rows, one chunk) touches 16 distinct 16-byte bank groups
+__device__ __forceinline__ uint32_t wide_off(int r, int c) {
+  return (uint32_t)(r * 2 * kWBk + ((c ^ ((r / (16 / kWChunks)) % kWChunks)) << 4));
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(512, 1) void proj_gemm_wide_kernel(const ProjGemmParams p) {
+  __shared__ __align__(16) unsigned char smem_raw[kWSmem];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+  const int tiles_j = (p.J + kWTile - 1) / kWTile;
+  const int64_t ti = blockIdx.x / tiles_j;
+  const int tj = (int)(blockIdx.x - ti * tiles_j);
+  const int64_t i0 = ti * kWTile;
+  const int j0 = tj * kWTile;
+  const int64_t nk = p.K / kWBk;
+
+  // ---- direct loads: wavefronts 0-3 load A (rows i0..), 4-7 B (rows j0..),
+  // kWPieces 1 KB pieces each per stage; lane l of piece q writes the 16
+  // bytes at 1024 q + 16 l of its operand tile: row (1024 q + 16 l) /
+  // (2 kWBk), stored chunk l % kWChunks, i.e. the source chunk that the
+  // swizzle puts there
+  const bool side_b = wave >= 4;
+  const bf16* src = side_b ? p.b : p.a;
+  const int64_t ld = side_b ? p.ldb : p.lda;
+  const int64_t r0 = side_b ? j0 : i0;
+  const int64_t nrows = side_b ? p.J : p.I;
+  uint32_t goff[kWPieces];
+#pragma unroll
+  for (int q = 0; q < kWPieces; ++q) {
+    const int byte = 1024 * (kWPieces * (wave & 3) + q) + 16 * lane;
+    const int r = byte / (2 * kWBk);
+    const int c = (lane % kWChunks) ^ ((r / (16 / kWChunks)) % kWChunks);
+    const int64_t row = r0 + r < nrows ? r0 + r : nrows - 1;  // rows past the end re-read the last (never stored)
+    goff[q] = (uint32_t)(((row - r0) * ld + 8 * c) * 2);
+  }
+  const char* gbase = reinterpret_cast<const char*>(src + r0 * ld);
+  const uint32_t lds0 = lds_addr(smem_raw);
+  const uint32_t dst0 = lds0 + (side_b ? kWOpBytes : 0u) + 1024u * (uint32_t)(kWPieces * (wave & 3));
+  auto buf = [&](int64_t kt) { return lds0 + ((uint32_t)kt % kWStages) * 2u * kWOpBytes; };
+  auto issue = [&](int64_t kt) {
+    const int64_t ks = kt < nk ? kt : nk - 1;  // past the end: the last stage again, into its idle buffer
+    const void* g = uniform_ptr(gbase + ks * (2 * kWBk));
+    const uint32_t d = dst0 + ((uint32_t)kt % kWStages) * 2u * kWOpBytes;
+#pragma unroll
+    for (int q = 0; q < kWPieces; ++q) dma16_async(g, goff[q], d + 1024u * q);
+  };
+
+  // ---- fragment reads: rows 32 x + (l % 32), chunk 2 ks + l / 32
+  uint32_t rd[kWKsteps];
+#pragma unroll
+  for (int ks = 0; ks < kWKsteps; ++ks) rd[ks] = wide_off(lane & 31, 2 * ks + (lane >> 5));
+  constexpr uint32_t kRowBlk = 32u * 2u * kWBk;  // bytes of 32 operand rows
+  const uint32_t a_row = (uint32_t)(4 * wm) * kRowBlk, b_row = kWOpBytes + (uint32_t)(2 * wn) * kRowBlk;
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+
+  // Fragments are read one k-step (16 reduction values) ahead, into the
+  // other of two register sets, between the MFMAs of the current k-step.
+  // The barrier that publishes stage kt+1 sits before the last k-step of
+  // stage kt, whose reads (those of kt+1's first k-step) follow it; by then
+  // every read of stage kt is done, so the loads of stage kt + kWStages go
+  // into its buffer right after that barrier.
+  typedef bf16x8 Frags[6];  // A rows 0..3, B columns 0..1 of one k-step
+  auto frag = [&](uint32_t T, int ks, int f) -> bf16x8 {
+    return f < 4 ? lds_ld16(T + a_row + kRowBlk * f + rd[ks]) : lds_ld16(T + b_row + kRowBlk * (f - 4) + rd[ks]);
+  };
+  // the eight MFMAs of a k-step from f, the six reads of the next one
+  // (stage buffer T, k-step ks) into g between them (after the last k-step
+  // they read an idle buffer, in bounds, and are not used)
+  auto kstep = [&](const Frags& f, uint32_t T, int ks, Frags& g) {
+    static_for<8>([&](auto mc) {
+      constexpr int m = decltype(mc)::value;
+      constexpr int i = m >> 1, j = m & 1;
+      acc[i][j] = mfma32(f[i], f[4 + j], acc[i][j]);
+      if constexpr (m < 6) g[m] = frag(T, ks, m);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
+#pragma unroll
+  for (int s0 = 0; s0 < kWStages; ++s0) issue(s0);
+  wait_vmcnt_lgkm0<kWPieces * (kWStages - 1)>();  // stage 0 has landed for this wavefront
+  lds_barrier();
+  Frags f0, f1;
+#pragma unroll
+  for (int m = 0; m < 6; ++m) f0[m] = frag(buf(0), 0, m);
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    const uint32_t T = buf(kt);
+    static_for<kWKsteps - 1>([&](auto kc) {
+      constexpr int ks = decltype(kc)::value;
+      if constexpr (ks % 2 == 0) kstep(f0, T, ks + 1, f1);
+      else kstep(f1, T, ks + 1, f0);
+    });
+    wait_vmcnt_lgkm0<kWPieces * (kWStages - 2)>();  // stage kt+1 has landed (later ones stay in flight)
+    lds_barrier();
+    issue(kt + kWStages);  // into stage kt's buffer, read completely before the barrier
+    kstep(f1, buf(kt + 1), 0, f0);  // the last k-step (kWKsteps is even); reads of stage kt+1's first
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // no direct load outlives the loop
+  __syncthreads();
+
+  // ---- epilogue: two passes of 128 rows staged in fp32 (the wavefronts of
+  // row half wm write in pass wm), then one 16-lane row per output row and
+  // head: lane l16 holds dims 8 l16 .. +7, its rotation partner (dims +-64)
+  // in lane l16 ^ 8 of the same DPP row.  Accumulator element v of lane l:
+  // row 8 (v/4) + 4 (l/32) + v%4, column l%32.
+  float* S = reinterpret_cast<float*>(smem_raw);
+  const int l16 = tid & 15;
+  const float sg = l16 < 8 ? -1.f : 1.f;
+  const int heads = p.J / kHeadDim;
+  for (int pass = 0; pass < 2; ++pass) {
+    if (wm == pass) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            S[(32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * kWStageLd + 64 * wn + 32 * j + (lane & 31)] =
+                acc[i][j][v];
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int rr = 0; rr < 2 * kWRows / 32; ++rr) {
+      const int t = (tid >> 4) + 32 * rr;  // row-head task: row t % 128, head half t / 128
+      const int r = t & (kWRows - 1), hsel = t >> 7;
+      const int head = 2 * tj + hsel;
+      const int64_t row = i0 + kWRows * pass + r;
+      if (head >= heads) continue;  // uniform over the DPP row
+      bf16* dst;
+      int hh, nh;
+      if (head < p.hq) {
+        dst = p.q; hh = head; nh = p.hq;
+      } else if (head < p.hq + p.hkv) {
+        dst = p.k; hh = head - p.hq; nh = p.hkv;
+      } else {
+        dst = p.v; hh = head - p.hq - p.hkv; nh = p.hkv;
+      }
+      const bool rot = p.rotate && head < p.hq + p.hkv;
+      const float* sr = S + r * kWStageLd + kHeadDim * hsel + 8 * l16;
+      const float4 x0 = *reinterpret_cast<const float4*>(sr);
+      const float4 x1 = *reinterpret_cast<const float4*>(sr + 4);
+      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      const int ps = (rot && row < p.I) ? p.pos[row] : -1;
+      float y[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float sn = 0.f, cs = 1.f;
+        if (ps >= 0) rope_sincos_fast(ps, p.freq.f[8 * (l16 & 7) + e], sn, cs);
+        const float xp = dpp_mov<0x128>(x[e]);  // row_ror:8, the partner lane l16 ^ 8
+        y[e] = fmaf(xp, sn * sg, x[e] * cs);
+      }
+      if (row < p.I) st16(dst + (row * nh + hh) * kHeadDim + 8 * l16, pack8(y[0], y[1], y[2], y[3], y[4], y[5], y[6], y[7]));
+    }
+    __syncthreads();
+  }
+}
+
 namespace {
 
 __device__ __forceinline__ void load8f(const bf16* p, float (&x)[8]) {
@@ -374,7 +565,10 @@ hipError_t launch_proj_gemm(const ProjGemmParams& p, bool a_imajor, bool b_imajo
   const int64_t tiles = ((p.I + kTile - 1) / kTile) * (p.J / kTile);
   if (tiles <= 0) return hipSuccess;
   const dim3 grid((unsigned)tiles), block(256);
-  if (epi == kProjEpiQkv && !a_imajor && !b_imajor)
+  if (epi == kProjEpiQkv && !a_imajor && !b_imajor && p.K % kWBk == 0) {
+    const int64_t wtiles = ((p.I + kWTile - 1) / kWTile) * ((p.J + kWTile - 1) / kWTile);
+    hipLaunchKernelGGL(proj_gemm_wide_kernel, dim3((unsigned)wtiles), dim3(512), 0, stream, p);
+  } else if (epi == kProjEpiQkv && !a_imajor && !b_imajor)
     hipLaunchKernelGGL((proj_gemm_kernel<false, false, kProjEpiQkv>), grid, block, 0, stream, p);
   else if (epi == kProjEpiPlain && !a_imajor && b_imajor)
     hipLaunchKernelGGL((proj_gemm_kernel<false, true, kProjEpiPlain>), grid, block, 0, stream, p);
