@@ -298,38 +298,110 @@ __global__ __launch_bounds__(256, 2) void proj_gemm_kernel(const ProjGemmParams 
 }
 
 // ------------------------------------------------------------------ wide
-// The forward product (both operands k-major, K % kWBk == 0) on 256 x 256
-// output tiles: eight wavefronts (two per SIMD), wavefront w computing the
-// 128 x 64 block at rows 128 (w / 4), columns 64 (w % 4) as 4 x 2 MFMA
-// accumulators, so each k-step's six operand fragments (6 KB) feed eight
-// MFMAs (0.75 KB of LDS reads per MFMA against 1 KB for the 64 x 64 blocks
-// above).  Operands go global -> LDS by direct loads (no register staging,
-// no LDS store instructions) into kWStages stages of kWBk reduction values,
-// one barrier per stage.
+// The same products on 256 x 256 output tiles when K % 64 == 0: eight
+// wavefronts (two per SIMD), wavefront w computing the 128 x 64 block at
+// rows 128 (w / 4), columns 64 (w % 4) as 4 x 2 MFMA accumulators, so each
+// k-step's six operand fragments (6 KB) feed eight MFMAs (0.75 KB of LDS
+// reads per MFMA against 1 KB for the 64 x 64 blocks above).  Operands go
+// global -> LDS by direct loads (no register staging, no LDS store
+// instructions) into two stages of 64 reduction values, one barrier per
+// stage.  Four wavefronts of 128 x 128 (0.5 KB per MFMA, one per SIMD)
+// measured slower.
 namespace {
 
 constexpr int kWTile = 256;                          // output tile rows and columns
 constexpr int kWBk = 64;                             // reduction values per stage
 constexpr int kWStages = 2;
-constexpr int kWChunks = kWBk / 8;                   // 16-byte chunks per operand row of a stage
 constexpr int kWKsteps = kWBk / 16;                  // MFMA k-steps per stage
-constexpr uint32_t kWOpBytes = kWTile * kWBk * 2;    // one operand of one stage
-constexpr int kWPieces = (int)(2 * kWOpBytes / 1024 / 8);  // 1 KB direct loads per wavefront and stage
+constexpr uint32_t kWOpBytes = kWTile * kWBk * 2;    // one operand of one stage (32 KB)
+constexpr int kWPieces = (int)(kWOpBytes / 1024 / 4);  // 1 KB direct loads per wavefront and stage
 constexpr int kWRows = 128;                          // epilogue rows staged per pass
 constexpr int kWStageLd = kWTile + 8;                // fp32 staging pitch
 constexpr int kWSmem = (int)(kWStages * 2 * kWOpBytes) > kWRows * kWStageLd * 4 ? (int)(kWStages * 2 * kWOpBytes)
                                                                                  : kWRows * kWStageLd * 4;
 
-// operand tile of a stage: 256 rows x kWBk reduction values (2 kWBk bytes
-// per row); 16-byte chunk c of row r sits at chunk c ^ ((r / (16 / kWChunks))
-// % kWChunks), so each group of 16 lanes of a fragment read (16 consecutive
-// rows, one chunk) touches 16 distinct 16-byte bank groups
-__device__ __forceinline__ uint32_t wide_off(int r, int c) {
-  return (uint32_t)(r * 2 * kWBk + ((c ^ ((r / (16 / kWChunks)) % kWChunks)) << 4));
-}
+// Operand tile of a stage, both layouts 32 KB, 32-row (or 32-column) block x
+// of the operand at byte 4096 x:
+//  * k-major: 256 rows x 64 reduction values, 128 B per row, 16-byte chunk c
+//    of row r at chunk c ^ ((r / 2) % 8), so each group of 16 lanes of a
+//    fragment read (16 consecutive rows, one chunk) touches 16 distinct
+//    16-byte bank groups;
+//  * i-major: two plane tiles (tile_off) of 64 reduction rows x 128 columns,
+//    columns 0..127 then 128..255, read with transposed 8-byte reads.
+__device__ __forceinline__ uint32_t wide_off(int r, int c) { return (uint32_t)(r * 128 + ((c ^ ((r >> 1) & 7)) << 4)); }
+
+// The direct loads of one wavefront: its share (pieces 8 sw .. 8 sw + 7 of
+// the 32) of one operand's stage, the operand rows (k-major) or columns
+// (i-major) r0 .. r0 + 255 of `src` (leading dimension ld, nrows of them).
+// Piece q lands at dbase + piece_dst(q): k-major pieces are 1 KB apart,
+// i-major ones (plane-tile loads m = 8 (sw % 2) + q of column half sw / 2)
+// at (q % 4) planes and q / 4 16-row groups from the wavefront's base.
+struct WideLoad {
+  uint32_t goff[kWPieces];
+  uint32_t dbase;       // wavefront-uniform
+  int64_t stage_bytes;  // global byte advance per stage
+  const char* gbase;
+  __device__ WideLoad(bool imajor, const bf16* src, int64_t ld, int64_t r0, int64_t nrows, int sw, int lane) {
+#pragma unroll
+    for (int q = 0; q < kWPieces; ++q) {
+      const int P = kWPieces * sw + q;
+      if (!imajor) {
+        // rows 8 P .. 8 P + 7; lane l: row 8 P + l / 8, stored chunk l % 8
+        const int r = 8 * P + (lane >> 3);
+        const int c = (lane & 7) ^ ((r >> 1) & 7);
+        const int64_t row = r0 + r < nrows ? r0 + r : nrows - 1;  // rows past the end re-read the last (never stored)
+        goff[q] = (uint32_t)(((row - r0) * ld + 8 * c) * 2);
+      } else {
+        // plane-tile load m of column half P / 16
+        const int half = P >> 4, m = P & 15;
+        const int k = dma_row<kWBk>(m, lane);
+        int64_t col = r0 + 128 * half + dma_col<kWBk>(m, lane);
+        col = col < nrows ? col : nrows - 8;  // columns past the end re-read the last eight (never stored)
+        goff[q] = (uint32_t)((k * ld + (col - r0)) * 2);
+      }
+    }
+    dbase = imajor ? 16384u * (uint32_t)(sw >> 1) + 2048u * (uint32_t)(sw & 1) : 8192u * (uint32_t)sw;
+    stage_bytes = imajor ? 2 * kWBk * ld : 2 * kWBk;
+    gbase = reinterpret_cast<const char*>(src + (imajor ? r0 : r0 * ld));
+  }
+};
+
+// Fragment reads of one operand: block x (32 rows or columns x 16
+// reduction values, k-step ks; lane l holding row/column l % 32 and
+// reduction values 16 ks + 8 (l / 32) + 0..7) is one 16-byte read
+// (k-major) or two transposed reads of four reduction rows each (i-major).
+template <bool kI>
+struct WideFrag {
+  uint32_t rd[kWKsteps];  // k-major: offset of block 0 per k-step
+  uint32_t lo, hi;        // i-major: the two transposed-read offsets of block 0, k-step 0
+  __device__ explicit WideFrag(int lane) {
+    const int h = lane >> 5, i = lane & 15;
+    if constexpr (!kI) {
+#pragma unroll
+      for (int ks = 0; ks < kWKsteps; ++ks) rd[ks] = wide_off(lane & 31, 2 * ks + h);
+      lo = hi = 0;
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < kWKsteps; ++ks) rd[ks] = 0;
+      lo = 2u * (uint32_t)tile_off<kWBk>(8 * h + (i >> 2), (lane & 16) + 4 * (i & 3));
+      hi = 2u * (uint32_t)tile_off<kWBk>(8 * h + 4 + (i >> 2), (lane & 16) + 4 * (i & 3));
+    }
+  }
+  template <int kKs>
+  __device__ __forceinline__ bf16x8 frag(uint32_t T, uint32_t x) const {
+    if constexpr (!kI) {
+      return lds_ld16(T + 4096u * x + rd[kKs]);
+    } else {
+      const uint32_t c = T + 4096u * x + 1024u * kKs;
+      const bf16x4 a = lds_ld_tr4(c + lo), b = lds_ld_tr4(c + hi);
+      return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+  }
+};
 
 }  // namespace
 
+template <bool kAI, bool kBI, int kEpi>
 __global__ __launch_bounds__(512, 1) void proj_gemm_wide_kernel(const ProjGemmParams p) {
   __shared__ __align__(16) unsigned char smem_raw[kWSmem];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -342,43 +414,28 @@ __global__ __launch_bounds__(512, 1) void proj_gemm_wide_kernel(const ProjGemmPa
   const int j0 = tj * kWTile;
   const int64_t nk = p.K / kWBk;
 
-  // ---- direct loads: wavefronts 0-3 load A (rows i0..), 4-7 B (rows j0..),
-  // kWPieces 1 KB pieces each per stage; lane l of piece q writes the 16
-  // bytes at 1024 q + 16 l of its operand tile: row (1024 q + 16 l) /
-  // (2 kWBk), stored chunk l % kWChunks, i.e. the source chunk that the
-  // swizzle puts there
+  // wavefronts 0-3 load A (rows / columns i0..), 4-7 B (j0..)
   const bool side_b = wave >= 4;
-  const bf16* src = side_b ? p.b : p.a;
-  const int64_t ld = side_b ? p.ldb : p.lda;
-  const int64_t r0 = side_b ? j0 : i0;
-  const int64_t nrows = side_b ? p.J : p.I;
-  uint32_t goff[kWPieces];
-#pragma unroll
-  for (int q = 0; q < kWPieces; ++q) {
-    const int byte = 1024 * (kWPieces * (wave & 3) + q) + 16 * lane;
-    const int r = byte / (2 * kWBk);
-    const int c = (lane % kWChunks) ^ ((r / (16 / kWChunks)) % kWChunks);
-    const int64_t row = r0 + r < nrows ? r0 + r : nrows - 1;  // rows past the end re-read the last (never stored)
-    goff[q] = (uint32_t)(((row - r0) * ld + 8 * c) * 2);
-  }
-  const char* gbase = reinterpret_cast<const char*>(src + r0 * ld);
+  const WideLoad ld = side_b ? WideLoad(kBI, p.b, p.ldb, j0, p.J, wave & 3, lane)
+                             : WideLoad(kAI, p.a, p.lda, i0, p.I, wave & 3, lane);
+  const uint32_t side_off = side_b ? kWOpBytes : 0u;
+  const WideFrag<kAI> opa(lane);
+  const WideFrag<kBI> opb(lane);
   const uint32_t lds0 = lds_addr(smem_raw);
-  const uint32_t dst0 = lds0 + (side_b ? kWOpBytes : 0u) + 1024u * (uint32_t)(kWPieces * (wave & 3));
   auto buf = [&](int64_t kt) { return lds0 + ((uint32_t)kt % kWStages) * 2u * kWOpBytes; };
   auto issue = [&](int64_t kt) {
     const int64_t ks = kt < nk ? kt : nk - 1;  // past the end: the last stage again, into its idle buffer
-    const void* g = uniform_ptr(gbase + ks * (2 * kWBk));
-    const uint32_t d = dst0 + ((uint32_t)kt % kWStages) * 2u * kWOpBytes;
+    const void* g = uniform_ptr(ld.gbase + ks * ld.stage_bytes);
+    const uint32_t d = buf(kt) + side_off + ld.dbase;
 #pragma unroll
-    for (int q = 0; q < kWPieces; ++q) dma16_async(g, goff[q], d + 1024u * q);
+    for (int q = 0; q < kWPieces; ++q) {
+      const uint32_t ck = 1024u * q, ci = 4096u * (q & 3) + 1024u * (q >> 2);
+      bool im;
+      if constexpr (kAI == kBI) im = kAI;
+      else im = side_b ? kBI : kAI;
+      dma16_async(g, ld.goff[q], d + (im ? ci : ck));
+    }
   };
-
-  // ---- fragment reads: rows 32 x + (l % 32), chunk 2 ks + l / 32
-  uint32_t rd[kWKsteps];
-#pragma unroll
-  for (int ks = 0; ks < kWKsteps; ++ks) rd[ks] = wide_off(lane & 31, 2 * ks + (lane >> 5));
-  constexpr uint32_t kRowBlk = 32u * 2u * kWBk;  // bytes of 32 operand rows
-  const uint32_t a_row = (uint32_t)(4 * wm) * kRowBlk, b_row = kWOpBytes + (uint32_t)(2 * wn) * kRowBlk;
 
   f32x16 acc[4][2];
 #pragma unroll
@@ -390,46 +447,72 @@ __global__ __launch_bounds__(512, 1) void proj_gemm_wide_kernel(const ProjGemmPa
   // other of two register sets, between the MFMAs of the current k-step.
   // The barrier that publishes stage kt+1 sits before the last k-step of
   // stage kt, whose reads (those of kt+1's first k-step) follow it; by then
-  // every read of stage kt is done, so the loads of stage kt + kWStages go
-  // into its buffer right after that barrier.
-  typedef bf16x8 Frags[6];  // A rows 0..3, B columns 0..1 of one k-step
-  auto frag = [&](uint32_t T, int ks, int f) -> bf16x8 {
-    return f < 4 ? lds_ld16(T + a_row + kRowBlk * f + rd[ks]) : lds_ld16(T + b_row + kRowBlk * (f - 4) + rd[ks]);
+  // every read of stage kt is done, so the loads of stage kt + 2 go into its
+  // buffer right after that barrier.
+  typedef bf16x8 Frags[6];  // A blocks 0..3, B blocks 0..1 of one k-step
+  const uint32_t xa = 4u * wm, xb = 2u * wn;
+  auto read = [&](uint32_t T, auto kc, int f) -> bf16x8 {
+    constexpr int ks = decltype(kc)::value;
+    return f < 4 ? opa.template frag<ks>(T, xa + f) : opb.template frag<ks>(T + kWOpBytes, xb + (f - 4));
   };
   // the eight MFMAs of a k-step from f, the six reads of the next one
   // (stage buffer T, k-step ks) into g between them (after the last k-step
   // they read an idle buffer, in bounds, and are not used)
-  auto kstep = [&](const Frags& f, uint32_t T, int ks, Frags& g) {
+  auto kstep = [&](const Frags& f, uint32_t T, auto kc, Frags& g) {
     static_for<8>([&](auto mc) {
       constexpr int m = decltype(mc)::value;
       constexpr int i = m >> 1, j = m & 1;
       acc[i][j] = mfma32(f[i], f[4 + j], acc[i][j]);
-      if constexpr (m < 6) g[m] = frag(T, ks, m);
+      if constexpr (m < 6) g[m] = read(T, kc, m);
       __builtin_amdgcn_sched_barrier(0);
     });
   };
 
-#pragma unroll
-  for (int s0 = 0; s0 < kWStages; ++s0) issue(s0);
-  wait_vmcnt_lgkm0<kWPieces * (kWStages - 1)>();  // stage 0 has landed for this wavefront
-  lds_barrier();
   Frags f0, f1;
+  if (nk > 0) {  // (an empty reduction loads nothing: the stage clamp needs one stage)
 #pragma unroll
-  for (int m = 0; m < 6; ++m) f0[m] = frag(buf(0), 0, m);
+    for (int s0 = 0; s0 < kWStages; ++s0) issue(s0);
+    wait_vmcnt_lgkm0<kWPieces * (kWStages - 1)>();  // stage 0 has landed for this wavefront
+    lds_barrier();
+#pragma unroll
+    for (int m = 0; m < 6; ++m) f0[m] = read(buf(0), std::integral_constant<int, 0>{}, m);
+  }
   for (int64_t kt = 0; kt < nk; ++kt) {
     const uint32_t T = buf(kt);
-    static_for<kWKsteps - 1>([&](auto kc) {
-      constexpr int ks = decltype(kc)::value;
-      if constexpr (ks % 2 == 0) kstep(f0, T, ks + 1, f1);
-      else kstep(f1, T, ks + 1, f0);
-    });
-    wait_vmcnt_lgkm0<kWPieces * (kWStages - 2)>();  // stage kt+1 has landed (later ones stay in flight)
+    kstep(f0, T, std::integral_constant<int, 1>{}, f1);
+    kstep(f1, T, std::integral_constant<int, 2>{}, f0);
+    kstep(f0, T, std::integral_constant<int, 3>{}, f1);
+    wait_vmcnt_lgkm0<kWPieces * (kWStages - 2)>();  // stage kt+1 has landed
     lds_barrier();
     issue(kt + kWStages);  // into stage kt's buffer, read completely before the barrier
-    kstep(f1, buf(kt + 1), 0, f0);  // the last k-step (kWKsteps is even); reads of stage kt+1's first
+    kstep(f1, buf(kt + 1), std::integral_constant<int, 0>{}, f0);  // the last k-step; reads of stage kt+1's first
   }
   __builtin_amdgcn_s_waitcnt(0);  // no direct load outlives the loop
   __syncthreads();
+
+  // accumulator element v of lane l: row 8 (v/4) + 4 (l/32) + v%4, column l%32
+  if constexpr (kEpi == kProjEpiPlain) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int64_t col = j0 + 64 * wn + 32 * j + (lane & 31);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int64_t row = i0 + 128 * wm + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          if (row < p.I && col < p.J) {
+            const int64_t at = row * p.ldc + col;
+            if (p.c_f32) {
+              float* c = static_cast<float*>(p.c);
+              c[at] = p.accumulate ? c[at] + acc[i][j][v] : acc[i][j][v];
+            } else {
+              static_cast<bf16*>(p.c)[at] = (bf16)acc[i][j][v];
+            }
+          }
+        }
+      }
+    return;
+  }
 
   // ---- epilogue: two passes of 128 rows staged in fp32 (the wavefronts of
   // row half wm write in pass wm), then one 16-lane row per output row and
@@ -565,9 +648,16 @@ hipError_t launch_proj_gemm(const ProjGemmParams& p, bool a_imajor, bool b_imajo
   const int64_t tiles = ((p.I + kTile - 1) / kTile) * (p.J / kTile);
   if (tiles <= 0) return hipSuccess;
   const dim3 grid((unsigned)tiles), block(256);
-  if (epi == kProjEpiQkv && !a_imajor && !b_imajor && p.K % kWBk == 0) {
-    const int64_t wtiles = ((p.I + kWTile - 1) / kWTile) * ((p.J + kWTile - 1) / kWTile);
-    hipLaunchKernelGGL(proj_gemm_wide_kernel, dim3((unsigned)wtiles), dim3(512), 0, stream, p);
+  if (p.K > 0 && p.K % kWBk == 0) {
+    const dim3 wgrid((unsigned)(((p.I + kWTile - 1) / kWTile) * ((p.J + kWTile - 1) / kWTile))), wblock(512);
+    if (epi == kProjEpiQkv && !a_imajor && !b_imajor)
+      hipLaunchKernelGGL((proj_gemm_wide_kernel<false, false, kProjEpiQkv>), wgrid, wblock, 0, stream, p);
+    else if (epi == kProjEpiPlain && !a_imajor && b_imajor)
+      hipLaunchKernelGGL((proj_gemm_wide_kernel<false, true, kProjEpiPlain>), wgrid, wblock, 0, stream, p);
+    else if (epi == kProjEpiPlain && a_imajor && b_imajor)
+      hipLaunchKernelGGL((proj_gemm_wide_kernel<true, true, kProjEpiPlain>), wgrid, wblock, 0, stream, p);
+    else
+      return hipErrorInvalidValue;
   } else if (epi == kProjEpiQkv && !a_imajor && !b_imajor)
     hipLaunchKernelGGL((proj_gemm_kernel<false, false, kProjEpiQkv>), grid, block, 0, stream, p);
   else if (epi == kProjEpiPlain && !a_imajor && b_imajor)

@@ -92,6 +92,12 @@ CASES = [
     (1000, 512, 8, 1, 5.0e5, 262143, torch.bfloat16, torch.float32),
     (257, 384, 6, 3, 0.0, 0, torch.float32, torch.bfloat16),
     (129, 128, 2, 2, 1.0e4, None, torch.bfloat16, torch.bfloat16),
+    # row counts that are multiples of 64 send dW to the 256 x 256 tile
+    # kernel too (dX and the forward take it whenever their reduction is a
+    # multiple of 64); output widths of 640 and 384 leave its last column
+    # tile part-filled, 320 rows its last row tile
+    (512, 384, 3, 1, 1.0e4, 4095, torch.bfloat16, torch.float32),
+    (320, 256, 4, 4, 5.0e5, 262143, torch.float32, torch.bfloat16),
 ]
 
 
