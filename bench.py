@@ -37,9 +37,9 @@ PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/c
 # calibration (profiles/traffic_eagle3-K3-L262144-cp8r0.md).  A figure only
 # applies while the kernel's source is the one that was measured.
 MEASURED_TRAFFIC = {
-    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "d0d63ec323720f5f", "bytes": 50306357928},
-    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "d0d63ec323720f5f", "bytes": 12011849103},
-    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "51b434b871aa004e", "bytes": 9075458882},
+    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "6cc2b451dd260598", "bytes": 18917582866},
+    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "6cc2b451dd260598", "bytes": 7807186278},
+    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "2bfe8b511fa00d56", "bytes": 7165812320},
 }
 
 def measured_traffic(kernel: str, workload: str, mode: str):
@@ -276,7 +276,7 @@ def bench_qkv(args):
                    "hidden": hidden, "hq": hq, "hkv": hkv, "rope_theta": theta},
         "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "ms": {"fwd": round(fwd_ms, 3), "bwd": round(bwd_ms, 3)},
-        "roofline": {"kernel": "proj_gemm_kernel (forward, rotary epilogue)", "bound": "mfma",
+        "roofline": {"kernel": "proj_gemm_wide_kernel (forward, rotary epilogue)", "bound": "mfma",
                      "achieved": round(achieved, 2), "peak": round(PEAK_BF16_TFLOPS, 1), "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                      "launches_per_step": len(parts), "launch_ms": round(fwd_ms / len(parts), 3)},
