@@ -15,8 +15,9 @@
 //                      transposing LDS reads, in the matching key order)
 // The tiles are software-pipelined: while the softmax of tile t runs on the
 // vector ALUs, the MFMAs compute S^T of tile t+1 and then O^T += V^T P^T of
-// tile t.  K/V tiles arrive by direct global-to-LDS loads into three
-// buffers (tile t+2 in flight).  O^T and Q^T live in the accumulation
+// tile t.  K/V tiles arrive by direct global-to-LDS loads into five
+// buffers (tiles t+2 and t+3 in flight, one barrier per two tiles).  O^T
+// and Q^T live in the accumulation
 // registers.  The running maximum used for the exponentials is only moved
 // (and O and the row sum rescaled) when a row's maximum grows by more than
 // kRescaleSlack in log2 units, so probabilities stay below 2^kRescaleSlack;
@@ -48,7 +49,7 @@ namespace {
 
 constexpr float kRescaleSlack = 8.f;  // log2 of the largest probability before a rescale
 constexpr int kFragAhead = 2;         // LDS operand fragments read ahead of their MFMAs
-constexpr int kKvBufs = 3;
+constexpr int kKvBufs = 5;  // tiles t-1 .. t+3 (see the walk)
 constexpr int kFwdRowBlocks = 1;  // 32-row blocks per wavefront (fwd_kernel's RB)
 
 }  // namespace
@@ -338,8 +339,10 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
     KvCursor cur = seek(p.step_first);
     if (cur.i < step_end) {
       KvCursor nxt = next(cur);
+      KvCursor nx2 = next(nxt);
       fetch(cur, 0);
       if (nxt.i < step_end) fetch(nxt, 1);
+      if (nx2.i < step_end) fetch(nx2, 2);
       __builtin_amdgcn_s_waitcnt(0);
       lds_barrier();
       f32x16 Sa[RB][2], Sb[RB][2];
@@ -356,29 +359,37 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
         for (int kb = 0; kb < 2; ++kb) vacc_settle(Sa[rb][kb]);
       tile_max(Sa, mx);
       int t = 0;
-      // tile t is in buffer t % 3; scores of tile t in Sa (t even) or Sb
-      auto step = [&](f32x16 (&Sc)[RB][2], f32x16 (&Sn)[RB][2]) {
-        const KvCursor n2 = next(nxt);
-        // with no tile t+2 the loads repeat tile t into the idle buffer
-        const KvCursor ld = n2.i < step_end ? n2 : cur;
-        const DmaTile d2 = dma_tile(ld, (t + 2) % kKvBufs);
+      // Tile t is in buffer t % 5; scores of tile t in Sa (t even) or Sb.
+      // Iteration t reads K of tile t+1 and V of tile t and loads tile t+3
+      // into the buffer of tile t-2, which no wavefront reads after the
+      // last barrier; only odd iterations wait for their loads and
+      // synchronise, which publishes tiles t+2 and t+3 for the next pair.
+      auto step = [&](f32x16 (&Sc)[RB][2], f32x16 (&Sn)[RB][2], auto sync) {
+        const KvCursor n3 = next(nx2);
+        // with no tile t+3 the loads repeat tile t into the idle buffer
+        const KvCursor ld = n3.i < step_end ? n3 : cur;
+        const DmaTile d3 = dma_tile(ld, (t + 3) % kKvBufs);
         if (cur.kv0 + kFwdKeys > cur.lim_lo) mask_tile(Sc, cur, mx);
         update_max(mx, m_eff);
         // with no tile t+1 the S^T MFMAs read a stale buffer and are discarded
         iterate(Sc, Sn, &kvbuf[(t + 1) % kKvBufs][0][0], &kvbuf[t % kKvBufs][1][0], m_eff, mx,
-                [&](int k) { fetch_piece(d2, k); });
-        wait_vmcnt_lgkm0<0>();  // tile t+2 has landed for this wavefront
-        lds_barrier();
+                [&](int k) { fetch_piece(d3, k); });
+        if constexpr (decltype(sync)::value) {
+          wait_vmcnt_lgkm0<0>();  // tiles t+2 and t+3 have landed for this wavefront
+          lds_barrier();
+        }
         cur = nxt;
-        nxt = n2;
+        nxt = nx2;
+        nx2 = n3;
         ++t;
       };
       while (true) {
-        step(Sa, Sb);
+        step(Sa, Sb, std::false_type{});
         if (cur.i >= step_end) break;
-        step(Sb, Sa);
+        step(Sb, Sa, std::true_type{});
         if (cur.i >= step_end) break;
       }
+      wait_vmcnt_lgkm0<0>();  // no direct load outlives the walk (after an even iteration some are in flight)
       mfma_drain();  // O^T complete before the epilogue reads it
     }
   }
