@@ -333,9 +333,10 @@ __device__ __forceinline__ uint32_t wide_off(int r, int c) { return (uint32_t)(r
 // The direct loads of one wavefront: its share (pieces 8 sw .. 8 sw + 7 of
 // the 32) of one operand's stage, the operand rows (k-major) or columns
 // (i-major) r0 .. r0 + 255 of `src` (leading dimension ld, nrows of them).
-// Piece q lands at dbase + piece_dst(q): k-major pieces are 1 KB apart,
-// i-major ones (plane-tile loads m = 8 (sw % 2) + q of column half sw / 2)
-// at (q % 4) planes and q / 4 16-row groups from the wavefront's base.
+// Piece q lands at dbase plus a per-piece constant (the kernel's issue):
+// k-major pieces are 1 KB apart, i-major ones (plane-tile loads m = 8 (sw %
+// 2) + q of column half sw / 2) q % 4 planes (4 KB) and q / 4 16-row groups
+// (1 KB) from the wavefront's base.
 struct WideLoad {
   uint32_t goff[kWPieces];
   uint32_t dbase;       // wavefront-uniform
