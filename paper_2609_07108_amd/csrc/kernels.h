@@ -139,6 +139,10 @@ struct ProjGemmParams {
 };
 
 hipError_t launch_proj_gemm(const ProjGemmParams& p, bool a_imajor, bool b_imajor, int epi, hipStream_t stream);
+// whether a product takes the 256 x 256 tile kernel (a non-zero reduction, a multiple of 64)
+bool proj_gemm_wide_ok(const ProjGemmParams& p);
+// dW = dY^T X (pw) and dX = dY W (px) of the backward in one launch, both on the 256 x 256 tile kernel
+hipError_t launch_proj_gemm_bwd_pair(const ProjGemmParams& pw, const ProjGemmParams& px, hipStream_t stream);
 hipError_t launch_proj_grad_pack(const void* dq, const void* dk, const void* dv, bool src_f32, bf16* dy,
                                  const int32_t* pos, int64_t rows, int hq, int hkv, bool rotate,
                                  const RopeFreqTable& freq, hipStream_t stream);

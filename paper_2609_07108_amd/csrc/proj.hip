@@ -402,15 +402,18 @@ struct WideFrag {
 
 }  // namespace
 
+// One 256 x 256 output tile (index `tile`, row-major over the output's
+// tiles) of the product in p, by the eight wavefronts of the workgroup.
+// fr: the lane's eight rotary frequencies (q / k / v epilogue only)
 template <bool kAI, bool kBI, int kEpi>
-__global__ __launch_bounds__(512, 1) void proj_gemm_wide_kernel(const ProjGemmParams p) {
-  __shared__ __align__(16) unsigned char smem_raw[kWSmem];
+__device__ __forceinline__ void wide_tile(const ProjGemmParams& p, int64_t tile, unsigned char* smem_raw,
+                                          const RopeFreq (&fr)[8]) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;
   const int tiles_j = (p.J + kWTile - 1) / kWTile;
-  const int64_t ti = blockIdx.x / tiles_j;
-  const int tj = (int)(blockIdx.x - ti * tiles_j);
+  const int64_t ti = tile / tiles_j;
+  const int tj = (int)(tile - ti * tiles_j);
   const int64_t i0 = ti * kWTile;
   const int j0 = tj * kWTile;
   const int64_t nk = p.K / kWBk;
@@ -524,6 +527,7 @@ __global__ __launch_bounds__(512, 1) void proj_gemm_wide_kernel(const ProjGemmPa
   const int l16 = tid & 15;
   const float sg = l16 < 8 ? -1.f : 1.f;
   const int heads = p.J / kHeadDim;
+
   for (int pass = 0; pass < 2; ++pass) {
     if (wm == pass) {
 #pragma unroll
@@ -562,7 +566,7 @@ __global__ __launch_bounds__(512, 1) void proj_gemm_wide_kernel(const ProjGemmPa
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float sn = 0.f, cs = 1.f;
-        if (ps >= 0) rope_sincos_fast(ps, p.freq.f[8 * (l16 & 7) + e], sn, cs);
+        if (ps >= 0) rope_sincos_fast(ps, fr[e], sn, cs);
         const float xp = dpp_mov<0x128>(x[e]);  // row_ror:8, the partner lane l16 ^ 8
         y[e] = fmaf(xp, sn * sg, x[e] * cs);
       }
@@ -570,6 +574,41 @@ __global__ __launch_bounds__(512, 1) void proj_gemm_wide_kernel(const ProjGemmPa
     }
     __syncthreads();
   }
+}
+
+template <bool kAI, bool kBI, int kEpi>
+__global__ __launch_bounds__(512, 1) void proj_gemm_wide_kernel(const ProjGemmParams p) {
+  __shared__ __align__(16) unsigned char smem_raw[kWSmem];
+  // the lane's frequencies (dim pairs 8 (l % 8) + e of lane l of a 16-lane
+  // row), picked with compile-time indices: with the parameter block also
+  // passed by reference, a run-time index into it makes the compiler keep a
+  // copy of the whole block in scratch memory
+  RopeFreq fr[8];
+  if constexpr (kEpi == kProjEpiQkv) {
+    const int fsel = threadIdx.x & 7;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      RopeFreq v = p.freq.f[e];
+#pragma unroll
+      for (int k = 1; k < 8; ++k)
+        if (fsel == k) v = p.freq.f[8 * k + e];
+      fr[e] = v;
+    }
+  }
+  wide_tile<kAI, kBI, kEpi>(p, blockIdx.x, smem_raw, fr);
+}
+
+// The backward's two products in one launch: the tiles of dW = dY^T X (pw,
+// both operands i-major, a reduction over all rows) first, then those of dX
+// = dY W (px).  dW has few, long tiles (384 at hidden 4096 and 48 heads, a
+// round and a half on 256 compute units); dX's many short ones then fill
+// the compute units that dW's last round leaves idle.
+__global__ __launch_bounds__(512, 1) void proj_gemm_wide_bwd_kernel(const ProjGemmParams pw, const ProjGemmParams px,
+                                                                    int64_t tiles_w) {
+  __shared__ __align__(16) unsigned char smem_raw[kWSmem];
+  const RopeFreq none[8] = {};
+  if ((int64_t)blockIdx.x < tiles_w) wide_tile<true, true, kProjEpiPlain>(pw, blockIdx.x, smem_raw, none);
+  else wide_tile<false, true, kProjEpiPlain>(px, (int64_t)blockIdx.x - tiles_w, smem_raw, none);
 }
 
 namespace {
@@ -649,7 +688,7 @@ hipError_t launch_proj_gemm(const ProjGemmParams& p, bool a_imajor, bool b_imajo
   const int64_t tiles = ((p.I + kTile - 1) / kTile) * (p.J / kTile);
   if (tiles <= 0) return hipSuccess;
   const dim3 grid((unsigned)tiles), block(256);
-  if (p.K > 0 && p.K % kWBk == 0) {
+  if (proj_gemm_wide_ok(p)) {
     const dim3 wgrid((unsigned)(((p.I + kWTile - 1) / kWTile) * ((p.J + kWTile - 1) / kWTile))), wblock(512);
     if (epi == kProjEpiQkv && !a_imajor && !b_imajor)
       hipLaunchKernelGGL((proj_gemm_wide_kernel<false, false, kProjEpiQkv>), wgrid, wblock, 0, stream, p);
@@ -667,6 +706,16 @@ hipError_t launch_proj_gemm(const ProjGemmParams& p, bool a_imajor, bool b_imajo
     hipLaunchKernelGGL((proj_gemm_kernel<true, true, kProjEpiPlain>), grid, block, 0, stream, p);
   else
     return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+bool proj_gemm_wide_ok(const ProjGemmParams& p) { return p.K > 0 && p.K % kWBk == 0; }
+
+hipError_t launch_proj_gemm_bwd_pair(const ProjGemmParams& pw, const ProjGemmParams& px, hipStream_t stream) {
+  const int64_t tw = ((pw.I + kWTile - 1) / kWTile) * ((pw.J + kWTile - 1) / kWTile);
+  const int64_t tx = ((px.I + kWTile - 1) / kWTile) * ((px.J + kWTile - 1) / kWTile);
+  if (tw + tx <= 0) return hipSuccess;
+  hipLaunchKernelGGL(proj_gemm_wide_bwd_kernel, dim3((unsigned)(tw + tx)), dim3(512), 0, stream, pw, px, tw);
   return hipGetLastError();
 }
 
@@ -789,36 +838,41 @@ extern "C" int branch_attn_qkv_bwd(void* stream, int64_t rows, int32_t hidden, i
   hipError_t e = ba::launch_proj_grad_pack(dq, dk, dv, grad_dtype == BA_DTYPE_F32, dy, pos, rows, hq, hkv, theta > 0.f,
                                            ft, s);
   if (e != hipSuccess) return proj_fail(BA_E_HIP, std::string("qkv gradient pack launch: ") + hipGetErrorString(e));
-  ba::ProjGemmParams p{};
   // dX [rows, hidden] = dY [rows, n] W [n, hidden]: A k-major, B i-major
-  p.a = dy;
-  p.lda = n;
-  p.b = static_cast<const ba::bf16*>(w);
-  p.ldb = hidden;
-  p.I = rows;
-  p.J = hidden;
-  p.K = n;
-  p.c = dx;
-  p.ldc = hidden;
-  p.c_f32 = dx_dtype == BA_DTYPE_F32;
-  p.accumulate = 0;
-  if ((e = ba::launch_proj_gemm(p, false, true, ba::kProjEpiPlain, s)) != hipSuccess)
-    return proj_fail(BA_E_HIP, std::string("qkv dX launch: ") + hipGetErrorString(e));
+  ba::ProjGemmParams px{};
+  px.a = dy;
+  px.lda = n;
+  px.b = static_cast<const ba::bf16*>(w);
+  px.ldb = hidden;
+  px.I = rows;
+  px.J = hidden;
+  px.K = n;
+  px.c = dx;
+  px.ldc = hidden;
+  px.c_f32 = dx_dtype == BA_DTYPE_F32;
+  px.accumulate = 0;
   // dW [n, hidden] (+)= dY^T X: A = dY read i-major, B = X read i-major,
   // reduction over the rows (ragged end allowed)
-  p = ba::ProjGemmParams{};
-  p.a = dy;
-  p.lda = n;
-  p.b = static_cast<const ba::bf16*>(x);
-  p.ldb = hidden;
-  p.I = n;
-  p.J = hidden;
-  p.K = rows;
-  p.c = dw;
-  p.ldc = hidden;
-  p.c_f32 = 1;
-  p.accumulate = accumulate_dw ? 1 : 0;
-  if ((e = ba::launch_proj_gemm(p, true, true, ba::kProjEpiPlain, s)) != hipSuccess)
+  ba::ProjGemmParams pw{};
+  pw.a = dy;
+  pw.lda = n;
+  pw.b = static_cast<const ba::bf16*>(x);
+  pw.ldb = hidden;
+  pw.I = n;
+  pw.J = hidden;
+  pw.K = rows;
+  pw.c = dw;
+  pw.ldc = hidden;
+  pw.c_f32 = 1;
+  pw.accumulate = accumulate_dw ? 1 : 0;
+  if (ba::proj_gemm_wide_ok(px) && ba::proj_gemm_wide_ok(pw)) {
+    if ((e = ba::launch_proj_gemm_bwd_pair(pw, px, s)) != hipSuccess)
+      return proj_fail(BA_E_HIP, std::string("qkv dW + dX launch: ") + hipGetErrorString(e));
+    return BA_OK;
+  }
+  if ((e = ba::launch_proj_gemm(px, false, true, ba::kProjEpiPlain, s)) != hipSuccess)
+    return proj_fail(BA_E_HIP, std::string("qkv dX launch: ") + hipGetErrorString(e));
+  if ((e = ba::launch_proj_gemm(pw, true, true, ba::kProjEpiPlain, s)) != hipSuccess)
     return proj_fail(BA_E_HIP, std::string("qkv dW launch: ") + hipGetErrorString(e));
   return BA_OK;
 }
