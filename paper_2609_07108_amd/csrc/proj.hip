@@ -520,8 +520,8 @@ __device__ __forceinline__ void wide_tile(const ProjGemmParams& p, int64_t tile,
 
   // ---- epilogue: two passes of 128 rows staged in fp32 (the wavefronts of
   // row half wm write in pass wm), then one 16-lane row per output row and
-  // head: lane l16 holds dims 8 l16 .. +7, its rotation partner (dims +-64)
-  // in lane l16 ^ 8 of the same DPP row.  Accumulator element v of lane l:
+  // both heads of the tile: lane l16 holds dims 8 l16 .. +7 of each, its
+  // rotation partner (dims +-64) in lane l16 ^ 8 of the same DPP row.  Accumulator element v of lane l:
   // row 8 (v/4) + 4 (l/32) + v%4, column l%32.
   float* S = reinterpret_cast<float*>(smem_raw);
   const int l16 = tid & 15;
@@ -540,37 +540,52 @@ __device__ __forceinline__ void wide_tile(const ProjGemmParams& p, int64_t tile,
                 acc[i][j][v];
     }
     __syncthreads();
-#pragma unroll 2
-    for (int rr = 0; rr < 2 * kWRows / 32; ++rr) {
-      const int t = (tid >> 4) + 32 * rr;  // row-head task: row t % 128, head half t / 128
-      const int r = t & (kWRows - 1), hsel = t >> 7;
-      const int head = 2 * tj + hsel;
+    // one row of both heads per task, the angles of a row once for both
+    for (int rr = 0; rr < kWRows / 32; ++rr) {
+      const int r = (tid >> 4) + 32 * rr;
       const int64_t row = i0 + kWRows * pass + r;
-      if (head >= heads) continue;  // uniform over the DPP row
-      bf16* dst;
-      int hh, nh;
-      if (head < p.hq) {
-        dst = p.q; hh = head; nh = p.hq;
-      } else if (head < p.hq + p.hkv) {
-        dst = p.k; hh = head - p.hq; nh = p.hkv;
-      } else {
-        dst = p.v; hh = head - p.hq - p.hkv; nh = p.hkv;
+      bf16* dst[2];
+      int hh[2], nh[2];
+      bool live[2], rot[2];
+#pragma unroll
+      for (int hs = 0; hs < 2; ++hs) {
+        const int head = 2 * tj + hs;
+        live[hs] = head < heads && row < p.I;
+        if (head < p.hq) {
+          dst[hs] = p.q; hh[hs] = head; nh[hs] = p.hq;
+        } else if (head < p.hq + p.hkv) {
+          dst[hs] = p.k; hh[hs] = head - p.hq; nh[hs] = p.hkv;
+        } else {
+          dst[hs] = p.v; hh[hs] = head - p.hq - p.hkv; nh[hs] = p.hkv;
+        }
+        rot[hs] = p.rotate && head < p.hq + p.hkv;
       }
-      const bool rot = p.rotate && head < p.hq + p.hkv;
-      const float* sr = S + r * kWStageLd + kHeadDim * hsel + 8 * l16;
-      const float4 x0 = *reinterpret_cast<const float4*>(sr);
-      const float4 x1 = *reinterpret_cast<const float4*>(sr + 4);
-      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      const int ps = (rot && row < p.I) ? p.pos[row] : -1;
-      float y[8];
+      float x[2][8];
+#pragma unroll
+      for (int hs = 0; hs < 2; ++hs) {
+        const float* sr = S + r * kWStageLd + kHeadDim * hs + 8 * l16;
+        const float4 x0 = *reinterpret_cast<const float4*>(sr);
+        const float4 x1 = *reinterpret_cast<const float4*>(sr + 4);
+        x[hs][0] = x0.x; x[hs][1] = x0.y; x[hs][2] = x0.z; x[hs][3] = x0.w;
+        x[hs][4] = x1.x; x[hs][5] = x1.y; x[hs][6] = x1.z; x[hs][7] = x1.w;
+      }
+      const int ps = ((rot[0] || rot[1]) && row < p.I) ? p.pos[row] : -1;
+      float y[2][8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float sn = 0.f, cs = 1.f;
         if (ps >= 0) rope_sincos_fast(ps, fr[e], sn, cs);
-        const float xp = dpp_mov<0x128>(x[e]);  // row_ror:8, the partner lane l16 ^ 8
-        y[e] = fmaf(xp, sn * sg, x[e] * cs);
+#pragma unroll
+        for (int hs = 0; hs < 2; ++hs) {
+          const float xp = dpp_mov<0x128>(x[hs][e]);  // row_ror:8, the partner lane l16 ^ 8
+          y[hs][e] = rot[hs] ? fmaf(xp, sn * sg, x[hs][e] * cs) : x[hs][e];
+        }
       }
-      if (row < p.I) st16(dst + (row * nh + hh) * kHeadDim + 8 * l16, pack8(y[0], y[1], y[2], y[3], y[4], y[5], y[6], y[7]));
+#pragma unroll
+      for (int hs = 0; hs < 2; ++hs)
+        if (live[hs])
+          st16(dst[hs] + (row * nh[hs] + hh[hs]) * kHeadDim + 8 * l16,
+               pack8(y[hs][0], y[hs][1], y[hs][2], y[hs][3], y[hs][4], y[hs][5], y[hs][6], y[hs][7]));
     }
     __syncthreads();
   }
