@@ -62,7 +62,10 @@ extern "C" {
  * BA_MODE_FUSED: one launch walks every ring step's KV block for a query
  *   tile, carrying the running (O, LSE) in registers (the online-softmax
  *   rescale is Eq. lse-merge applied between steps), then merges the
- *   branch-local part with Eq. lse-merge and writes the result. */
+ *   branch-local part with Eq. lse-merge and writes the result; the
+ *   backward's dQ likewise.
+ * In both, the backward's dK/dV (of each ring step's KV block) is launched
+ * once per ring step. */
 #define BA_MODE_PER_STEP 0
 #define BA_MODE_FUSED 1
 /* BA_MODE_AUTO: the plan picks one of the two.  Per-step when every ring
