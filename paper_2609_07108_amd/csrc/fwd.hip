@@ -203,10 +203,43 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
       for (int k = 0; k < 4 * RB; ++k) fetch_piece(d, k);
     };
 
+    // ---- LDS fragment reads at a per-tile base address plus a lane
+    // constant plus a compile-time offset.  In the plane-tile layout
+    // (tile_off) the byte offset of K row 32 kb + qi, dims 16 c + 8 half is
+    //   4096 (c / 2) + 2048 kb + 64 qi + 16 ((2 (c % 2) + half) ^ (qi / 4 % 4)),
+    // so the lane part takes one of two values (c even / odd); a transposed
+    // V read (ld_tr8 with rows 16 t4 + 4 half + i/4 and 16 t4 + 8 + 4 half +
+    // i/4, columns 32 dt + (l & 16) + 4 (i % 4), i = l % 16) is at
+    //   4096 dt + 1024 t4 + (lane part, one for each of the two row groups).
+    const uint32_t q2 = (uint32_t)((qi >> 2) & 3);
+    const uint32_t kl0 = 64u * qi + ((((uint32_t)half) ^ q2) << 4);
+    const uint32_t kl1 = 64u * qi + ((((uint32_t)half ^ 2u) ^ q2) << 4);
+    const uint32_t vl_lo = 2u * (uint32_t)tile_off<kFwdKeys>(4 * half + ((lane & 15) >> 2), (lane & 16) + 4 * (lane & 3));
+    const uint32_t vl_hi = 2u * (uint32_t)tile_off<kFwdKeys>(8 + 4 * half + ((lane & 15) >> 2), (lane & 16) + 4 * (lane & 3));
+    // The per-tile bases (tile address + lane part) are formed once per tile
+    // and hidden from the compiler, which would otherwise fold each read's
+    // constant into the tile address first and add the lane part per read.
+    struct KBase {
+      uint32_t b0, b1;
+    };
+    struct VBase {
+      uint32_t lo, hi;
+    };
+    auto k_base = [&](uint32_t ks) {
+      KBase k{ks + kl0, ks + kl1};
+      asm volatile("" : "+v"(k.b0), "+v"(k.b1));
+      return k;
+    };
+    auto v_base = [&](uint32_t vs) {
+      VBase v{vs + vl_lo, vs + vl_hi};
+      asm volatile("" : "+v"(v.lo), "+v"(v.hi));
+      return v;
+    };
     // ---- S^T of a tile: fragment f = 8 kb + c (keys 32 kb.., dims 16 c..)
     // feeds both row blocks
-    auto s_frag = [&](const bf16* ks, int f) -> bf16x8 {
-      return ld16(&ks[tile_off<kFwdKeys>(32 * (f >> 3) + qi, 16 * (f & 7) + 8 * half)]);
+    auto s_frag = [&](const KBase& k, int f) -> bf16x8 {
+      const int kb = f >> 3, c = f & 7;
+      return lds_ld16(((c & 1) ? k.b1 : k.b0) + 4096u * (uint32_t)(c >> 1) + 2048u * (uint32_t)kb);
     };
     auto s_mfma = [&](f32x16 (&S)[RB][2], int f, int rb, const bf16x8& a) {
       const int kb = f >> 3, c = f & 7;
@@ -216,9 +249,11 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
     // ---- O^T += V^T P^T: fragment g = 4 t4 + dt (keys 16 t4.., dims 32 dt..);
     // a lane of half h holds keys 16 t4 + 4h + {0..3} and 16 t4 + 8 + 4h +
     // {0..3} in its S^T registers and reads V^T from exactly those rows
-    auto v_frag = [&](const bf16* vs, int g) -> bf16x8 {
+    auto v_frag = [&](const VBase& v, int g) -> bf16x8 {
       const int t4 = g >> 2, dt = g & 3;
-      return ld_tr8<kFwdKeys>(vs, 32 * dt, 16 * t4 + 4 * half, 16 * t4 + 8 + 4 * half, lane);
+      const uint32_t o = 4096u * (uint32_t)dt + 1024u * (uint32_t)t4;
+      const bf16x4 lo = lds_ld_tr4(v.lo + o), hi = lds_ld_tr4(v.hi + o);
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     };
 
     // maximum of S^T (raw scores) over this lane's 32 keys of a tile (the
@@ -243,7 +278,7 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
     // j >= 32 -> V^T fragment (j-32)/2, row block j%2.  Softmax element e
     // (t4 = e/16, row block (e/8)%2, accumulator slot 8 (t4%2) + e%8 of key
     // block t4/2) in slot 52e/64, ahead of the MFMAs of key block t4.
-    auto iterate = [&](f32x16 (&Sc)[RB][2], f32x16 (&Sn)[RB][2], const bf16* ks_n, const bf16* vs_c,
+    auto iterate = [&](f32x16 (&Sc)[RB][2], f32x16 (&Sn)[RB][2], uint32_t ks_n, uint32_t vs_c,
                        const float (&m_eff)[RB], float (&mx_n)[RB], auto&& issue_piece) {
       typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
       bf16x8 fq[kFragAhead + 1];
@@ -252,7 +287,9 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
       // [row block][t4] -> the B operand of the t4-th O^T MFMA
       u32x4 pk[RB][4];
       float pv[RB][4][8];
-      auto frag = [&](int f) -> bf16x8 { return f < 16 ? s_frag(ks_n, f) : v_frag(vs_c, f - 16); };
+      const KBase kbn = k_base(ks_n);
+      const VBase vbc = v_base(vs_c);
+      auto frag = [&](int f) -> bf16x8 { return f < 16 ? s_frag(kbn, f) : v_frag(vbc, f - 16); };
       auto element = [&](int e) {
         const int t4 = e / (8 * RB), rb = (e >> 3) % RB, i = e & 7;
         const float x = Sc[rb][t4 >> 1][8 * (t4 & 1) + i];
@@ -350,7 +387,7 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
       // prologue: S^T of the first tile
       static_for<16 * RB>([&](auto jc) {
         constexpr int j = decltype(jc)::value;
-        s_mfma(Sa, j / RB, j % RB, s_frag(&kvbuf[0][0][0], j / RB));
+        s_mfma(Sa, j / RB, j % RB, s_frag(k_base(kv_lds), j / RB));
       });
       mfma_drain();  // the scores are read by the vector ALUs next
 #pragma unroll
@@ -372,7 +409,8 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
         if (cur.kv0 + kFwdKeys > cur.lim_lo) mask_tile(Sc, cur, mx);
         update_max(mx, m_eff);
         // with no tile t+1 the S^T MFMAs read a stale buffer and are discarded
-        iterate(Sc, Sn, &kvbuf[(t + 1) % kKvBufs][0][0], &kvbuf[t % kKvBufs][1][0], m_eff, mx,
+        iterate(Sc, Sn, kv_lds + (uint32_t)((t + 1) % kKvBufs) * 2u * kTileBytes,
+                kv_lds + (uint32_t)(t % kKvBufs) * 2u * kTileBytes + kTileBytes, m_eff, mx,
                 [&](int k) { fetch_piece(d3, k); });
         if constexpr (decltype(sync)::value) {
           wait_vmcnt_lgkm0<0>();  // tiles t+2 and t+3 have landed for this wavefront
