@@ -192,7 +192,6 @@ constexpr int b_slot(int e) { return 17 + (e * 38) / 64; }
 
 __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(16))) KvLds sm;
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
   const BwdTile tile = p.tiles[blockIdx.x];
@@ -388,7 +387,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
           const int lim = c == 0 ? sp[rb][q].x : c == 1 ? sp[rb][q].y : c == 2 ? sp[rb][q].z : sp[rb][q].w;
           pr = kpos[kb] <= lim ? pr : 0.f;
         }
-        if (v & 1) pn[rb][kb][v >> 3][(v & 7) >> 1] = __builtin_bit_cast(uint32_t, bf16x2{(bf16)prv, (bf16)pr});
+        if (v & 1) pn[rb][kb][v >> 3][(v & 7) >> 1] = pack_bf16x2(prv, pr);
         else prv = pr;
       };
       auto mfma = [&](int j, const bf16x8& a) {
@@ -526,7 +525,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
       auto element = [&](int e) {
         const int t = e >> 4, rb = t >> 1, tt = t & 1, kb = (e >> 3) & 1, i = e & 7, v = 8 * tt + i;
         const float ds = (float)pf[rb][kb][tt][i] * dp[rb][kb][v];
-        if (i & 1) dsf[rb][kb][tt][i >> 1] = __builtin_bit_cast(uint32_t, bf16x2{(bf16)dsv, (bf16)ds});
+        if (i & 1) dsf[rb][kb][tt][i >> 1] = pack_bf16x2(dsv, ds);
         else dsv = ds;
       };
       auto mfma = [&](int j, const bf16x8& a) {
@@ -678,7 +677,6 @@ template <int MODE>
 __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
   // [buffer][K, V] plane tiles of 64 keys (see tile_off)
   __shared__ __attribute__((aligned(16))) bf16 kvbuf[kDqBufs][2][kFwdKeys * kHeadDim];
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
   const FwdTile tile = p.qtiles[blockIdx.x];
@@ -898,7 +896,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
       const float pr = fast_exp2(__builtin_fmaf(S[rb][v], p.scale_log2, nl2[rb]));
       const float ds = pr * P[rb][v];
       if (i & 1) {
-        uint32_t w = __builtin_bit_cast(uint32_t, bf16x2{(bf16)prv, (bf16)ds});
+        uint32_t w = pack_bf16x2(prv, ds);
         asm volatile("" : "+v"(w));  // packed in this slot, not next to the MFMA that reads it
         D[rb][tt][i >> 1] = w;
       } else {

@@ -110,6 +110,15 @@ __device__ __forceinline__ bf16x8 pack8(float a0, float a1, float a2, float a3, 
   return r;
 }
 
+// Two floats rounded to bf16 (nearest even) in one 32-bit word, lo in the
+// low half: one v_cvt_pk_bf16_f32 (two scalar casts combined afterwards can
+// compile to a conversion each plus a byte permute).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 b16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, b16x2));
+}
+
 __device__ __forceinline__ bf16x4 pack4(float a0, float a1, float a2, float a3) {
   bf16x4 r;
   r[0] = (bf16)a0; r[1] = (bf16)a1; r[2] = (bf16)a2; r[3] = (bf16)a3;

@@ -280,7 +280,6 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
     // block t4/2) in slot 52e/64, ahead of the MFMAs of key block t4.
     auto iterate = [&](f32x16 (&Sc)[RB][2], f32x16 (&Sn)[RB][2], uint32_t ks_n, uint32_t vs_c,
                        const float (&m_eff)[RB], float (&mx_n)[RB], auto&& issue_piece) {
-      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
       bf16x8 fq[kFragAhead + 1];
       typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
       // packed P^T as bf16 pairs, converted in the element's own slot:
@@ -296,7 +295,7 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
         const float pr = fast_exp2(__builtin_fmaf(x, p.scale_log2, -m_eff[rb]));
         pv[rb][t4][i] = pr;
         lsum[rb] += pr;  // fp32 probabilities: the LSE bar is tighter than bf16 rounding
-        if (i & 1) pk[rb][t4][i >> 1] = __builtin_bit_cast(uint32_t, bf16x2{(bf16)pv[rb][t4][i - 1], (bf16)pr});
+        if (i & 1) pk[rb][t4][i >> 1] = pack_bf16x2(pv[rb][t4][i - 1], pr);
       };
       auto pa = [&](int rb, int t4) {
         return __builtin_bit_cast(bf16x8, pk[rb][t4]);
