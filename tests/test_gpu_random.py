@@ -5,6 +5,10 @@ some empty), per sequence no branches / an EAGLE-3 chain of random depth / DFlas
 random size (one or two per window, with or without main queries), a GQA
 ratio, the branch-array layout, the ring schedule, the gradient dtype and
 rotary embedding on or off.  Same tolerances as the hand-picked cases.
+A second generator draws sequences of up to 2048 tokens (walks of up to 32
+key tiles per ring block), DFlash blocks up to 64 and the plan's own
+schedule choice as a third mode; its seeds are a spread over CP sizes 1-8,
+schedules, layouts and rotary settings whose oracle finishes in seconds.
 """
 
 import numpy as np
@@ -56,6 +60,38 @@ def draw_case(seed):
     return prob, opts
 
 
+def draw_long_case(seed):
+    rng = np.random.default_rng(50000 + seed)
+    C = int(rng.choice([1, 2, 3, 4, 8]))
+    r = int(rng.integers(C))
+    ns = int(rng.integers(1, 4))
+    lens, spec, has_main = [], [], []
+    for _ in range(ns):
+        L = 2 * C * int(rng.integers(0, max(2, 2048 // (2 * C))))
+        kind = rng.choice(["none", "eagle", "dflash"], p=[0.2, 0.45, 0.35])
+        if kind == "eagle" and L:
+            spec.append(("eagle", int(rng.integers(1, 9))))
+            has_main.append(True)
+        elif kind == "dflash" and L >= 16:
+            bs = int(rng.choice([4, 8, 16, 32, 64]))
+            nb = int(rng.integers(1, 3))
+            window = min(bs * int(rng.integers(2, 5)), L)
+            spec.append(("dflash", bs, window, nb))
+            has_main.append(bool(rng.integers(2)))
+        else:
+            spec.append(None)
+            has_main.append(True)
+        lens.append(L)
+    hq, hkv = HEADS[int(rng.integers(len(HEADS)))]
+    prob = W.custom(lens, spec, hq=hq, hkv=hkv, cp_size=C, cp_rank=r, seed=60000 + seed, has_main=has_main,
+                    anchor_seed=70000 + seed, name=f"random_long{seed}")
+    opts = dict(layout=str(rng.choice(["group", "depth"])),
+                mode=str(rng.choice(["per_step", "fused", "auto"])),
+                grad=torch.float32 if rng.integers(2) else torch.bfloat16,
+                theta=float(rng.choice([0.0, 1.0e4, 5.0e5])))
+    return prob, opts
+
+
 @pytest.fixture(scope="module")
 def cuda():
     if not torch.cuda.is_available():
@@ -64,10 +100,8 @@ def cuda():
     return torch.device("cuda:0")
 
 
-@pytest.mark.parametrize("seed", range(16))
-def test_random_problem_parity(cuda, seed):
-    prob, o = draw_case(seed)
-    print(f"[random {seed}] lens {list(np.diff(prob.cu_seqlens))} C={prob.cp_size} r={prob.cp_rank} "
+def run_case(tag, prob, o):
+    print(f"[{tag}] lens {list(np.diff(prob.cu_seqlens))} C={prob.cp_size} r={prob.cp_rank} "
           f"heads {prob.hq}/{prob.hkv} groups {len(prob.g_len)} {o}", flush=True)
     mq, bq = oracle.select_queries(prob)
     if len(mq) + len(bq) == 0:
@@ -82,7 +116,19 @@ def test_random_problem_parity(cuda, seed):
         ref_f = oracle.forward(prob, *args, mq, bq)
         ref_b = oracle.backward(prob, *args, dom, dob, mq, bq)
     share = RS.build_share(prob, device="cuda", layout=o["layout"], rope_theta=o["theta"])
-    mode = B.BA_MODE_FUSED if o["mode"] == "fused" else B.BA_MODE_PER_STEP
+    mode = {"fused": B.BA_MODE_FUSED, "per_step": B.BA_MODE_PER_STEP, "auto": B.BA_MODE_AUTO}[o["mode"]]
     got_f, got_b, _ = H.gpu_bwd(share, mode, mq, bq, grad_dtype=o["grad"])
     H.assert_fwd_close(got_f, ref_f)
     H.assert_bwd_close(got_b, ref_b)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_problem_parity(cuda, seed):
+    prob, o = draw_case(seed)
+    run_case(f"random {seed}", prob, o)
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3, 5, 7, 8, 13, 14, 24, 30, 33, 35, 40, 46, 52, 56])
+def test_random_long_problem_parity(cuda, seed):
+    prob, o = draw_long_case(seed)
+    run_case(f"random long {seed}", prob, o)
