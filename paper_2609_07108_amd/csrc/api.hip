@@ -155,6 +155,8 @@ extern "C" int branch_attn_fwd(void* stream_, const ba_plan* plan, int32_t mode,
   p.groups = reinterpret_cast<const GroupInfo*>(c.ws + c.w.tables + P.off_groups);
   p.tiles = reinterpret_cast<const FwdTile*>(c.ws + c.w.tables + P.off_fwd);
   p.num_tiles = (int32_t)P.fwd_tiles.size();
+  p.br_keys = reinterpret_cast<const int32_t*>(c.ws + c.w.tables + P.off_br_keys);
+  p.tok_bslot = reinterpret_cast<const int32_t*>(c.ws + c.w.tables + P.off_bslot);
   p.C = P.cp_size;
   p.rank = P.cp_rank;
   p.hq = P.hq;

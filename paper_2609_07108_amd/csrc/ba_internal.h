@@ -101,7 +101,20 @@ struct FwdTile {
   int32_t tok_begin;
   int32_t ntok;
   int32_t kvh;
+  // branch-local keys of the tile's tokens: rows br_keys[bk_off ..
+  // bk_off + bk_n) of the branch K/V arrays, each group's keys consecutive
+  // (a token's group starts at its tok_bslot); bk_n = -1: more than
+  // kBrSlots keys, the rows read their keys from global memory instead
+  int32_t bk_off;
+  int32_t bk_n;
 };
+
+// LDS staging of a forward tile's branch-local keys in the fused epilogue:
+// K rows then V rows of up to kBrSlots keys, kBrPitch bytes apart (256 bytes
+// of data plus 16 of padding, so rows of different keys start in different
+// bank groups)
+constexpr int32_t kBrSlots = 288;
+constexpr int32_t kBrPitch = 272;
 
 struct BwdTile {
   int32_t step;     // ring step block j
@@ -165,6 +178,8 @@ struct Plan {
   std::vector<TokInfo> toks;
   std::vector<GroupInfo> groups;
   std::vector<FwdTile> fwd_tiles;
+  std::vector<int32_t> br_keys;        // branch key rows of the forward tiles (see FwdTile)
+  std::vector<int32_t> tok_bslot;      // per token: first slot of its group's keys in its tile, -1 main
   std::vector<BwdTile> bwd_tiles;      // grouped by ring step i = 0..C-1
   std::vector<int32_t> bwd_step_off;   // [C+1] tile range of each ring step
   std::vector<KvSplit> kv_splits;      // keys whose items write partial sums
@@ -172,6 +187,7 @@ struct Plan {
   // packed image of the tables and their byte offsets inside it
   std::vector<uint8_t> image;
   size_t off_seqs = 0, off_toks = 0, off_groups = 0, off_fwd = 0, off_bwd = 0, off_splits = 0;
+  size_t off_br_keys = 0, off_bslot = 0;
   // rotary position embedding (off while rope_theta == 0): positions of the
   // rows of every ring-step block ([C][n_local], block j = rank j's local
   // rows), of this rank's main rows that are queries and of the branch rows

@@ -119,6 +119,17 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, b16x2));
 }
 
+// c + <a, b> over eight bf16 pairs with fp32 products and sums, as four
+// packed two-term dot products (v_dot2c_f32_bf16) instead of sixteen
+// conversions and eight fused multiply-adds
+__device__ __forceinline__ float dot8_bf16(const bf16x8& a, const bf16x8& b, float c) {
+  c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 0, 1), __builtin_shufflevector(b, b, 0, 1), c, false);
+  c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 2, 3), __builtin_shufflevector(b, b, 2, 3), c, false);
+  c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 4, 5), __builtin_shufflevector(b, b, 4, 5), c, false);
+  c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 6, 7), __builtin_shufflevector(b, b, 6, 7), c, false);
+  return c;
+}
+
 __device__ __forceinline__ bf16x4 pack4(float a0, float a1, float a2, float a3) {
   bf16x4 r;
   r[0] = (bf16)a0; r[1] = (bf16)a1; r[2] = (bf16)a2; r[3] = (bf16)a3;
@@ -244,6 +255,12 @@ __device__ __forceinline__ uint32_t lds_lane_addr(const void* p) {
 }
 __device__ __forceinline__ bf16x8 lds_ld16(uint32_t a) {
   return *(const __attribute__((address_space(3))) bf16x8*)(uintptr_t)a;
+}
+__device__ __forceinline__ bf16x4 lds_ld8(uint32_t a) {
+  return *(const __attribute__((address_space(3))) bf16x4*)(uintptr_t)a;
+}
+__device__ __forceinline__ void lds_st16(uint32_t a, const bf16x8& v) {
+  *(__attribute__((address_space(3))) bf16x8*)(uintptr_t)a = v;
 }
 __device__ __forceinline__ bf16x4 lds_ld_tr4(uint32_t a) {
   const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(uintptr_t)a);

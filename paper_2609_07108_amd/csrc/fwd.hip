@@ -36,7 +36,12 @@
 // FUSED and the finalize kernel compute the branch-local partial of every
 // branch row (chain members 0..i, or the whole block; at most 64 keys, on
 // the vector ALUs), merge it with the main partial by Eq. lse-merge and
-// write bf16 O and the natural-log LSE.
+// write bf16 O and the natural-log LSE.  In FUSED the tile's branch keys
+// (each group's once, listed by the planner) are first copied into the LDS
+// that the walk has freed, so a row's keys cost LDS reads rather than a
+// chain of dependent global loads per key; the rows then take them eight at
+// a time (packed bf16 dot products for the scores, one online-softmax step
+// per batch).
 #include <type_traits>
 
 #include "ba_internal.h"
@@ -441,14 +446,51 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) l_tot[rb] = lsum[rb] + xor32(lsum[rb]);
 
+  // FUSED: the branch-local keys of the tile's tokens (each group's once,
+  // listed by the planner) staged in the LDS that the key walk has freed, K
+  // rows then V rows; a tile with more than kBrSlots of them (bk_n < 0)
+  // reads them from global memory per row instead
+  const bool staged = MODE == kModeFused && tile.bk_n > 0;
+  const uint32_t br_lds = lds_addr(&kvbuf[0][0][0]);
+  if (staged) {
+    constexpr int kThreads = 512 / RB;
+    constexpr int kUnroll = 4;
+    __syncthreads();  // every wavefront is past its last read of the K/V buffers
+    const int nch = tile.bk_n * 32;  // 16-byte chunks: 16 of K and 16 of V per key
+    // the thread index recomputed (no register holds it across the walk)
+    const int t_id = 64 * wave + (int)__lane_id();
+    for (int c0 = t_id; c0 < nch; c0 += kUnroll * kThreads) {
+      int32_t krow[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) krow[u] = p.br_keys[tile.bk_off + (min(c0 + u * kThreads, nch - 1) >> 5)];
+      bf16x8 v[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int part = min(c0 + u * kThreads, nch - 1) & 31;
+        v[u] = ld16((part < 16 ? p.k_br : p.v_br) + (int64_t)krow[u] * kv_row_stride + tile.kvh * kHeadDim +
+                    8 * (part & 15));
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int c = c0 + u * kThreads;
+        const int part = c & 31;
+        if (c < nch)
+          lds_st16(br_lds + (part < 16 ? 0u : (uint32_t)(kBrSlots * kBrPitch)) + (uint32_t)(c >> 5) * kBrPitch +
+                       16u * (uint32_t)(part & 15),
+                   v[u]);
+      }
+    }
+    __syncthreads();
+  }
+
   auto finish = [&](int rb) {
     const int64_t acc_row = (int64_t)(tile.tok_begin + (32 * RB * wave + 32 * rb + qi) / p.G) * p.hq + head[rb];
-    f32x16 st_o[4];
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt) st_o[dt] = o[rb][dt];
 
     if (MODE == kModeStep) {
       if (!valid[rb]) return;
+      f32x16 st_o[4];
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) st_o[dt] = o[rb][dt];
       float* oacc = p.o_acc + acc_row * kHeadDim;
       if (l_tot[rb] > 0.f) {
         const float lse2 = m_use[rb] + __log2f(l_tot[rb]);
@@ -503,29 +545,84 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
       return;
     }
 
-    // main-sequence partial: normalised output in st_o, LSE (log2) in lse_m
-    float lse_m;
+    // main-sequence partial: LSE (log2) in lse_m; O^T stays in the
+    // accumulation registers until the output is written, normalised by
+    // inv there
+    float lse_m, inv = 0.f;
     if (l_tot[rb] > 0.f) {
       lse_m = m_use[rb] + __log2f(l_tot[rb]);
-      const float inv = 1.f / l_tot[rb];
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) st_o[dt] *= inv;
+      inv = 1.f / l_tot[rb];
     } else {
       lse_m = -INFINITY;
     }
 
     // ---- branch-local partial (vector ALUs; at most 64 keys per row)
     int nb = 0;
+    int bslot = 0;
     GroupInfo gi{0, 1, 0, 0, 0, 0, {0, 0}};
     if (valid[rb] && tk[rb].grp >= 0) {
       gi = p.groups[tk[rb].grp];
       nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk[rb].gidx + 1 : gi.len;
+      if (staged) bslot = p.tok_bslot[tile.tok_begin + (32 * RB * wave + 32 * rb + qi) / p.G];
     }
     float mb = -INFINITY, lb = 0.f;
     f32x16 ob[4];
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) ob[dt] = f32x16{};
-    for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
+    if (staged) {
+      // keys in batches of eight from the staged rows: the row's Q read once,
+      // one online-softmax step per batch; a lane past its keys reads a
+      // valid slot and gives it probability 0
+      constexpr int kBatch = 8;
+      const uint32_t kb0 = br_lds + (uint32_t)bslot * kBrPitch + 16u * (uint32_t)half;
+      const uint32_t vb0 = br_lds + (uint32_t)(kBrSlots * kBrPitch) + (uint32_t)bslot * kBrPitch + 8u * (uint32_t)half;
+      for (int b0 = 0; b0 < BA_MAX_GROUP_LEN; b0 += kBatch) {
+        if (__ballot(b0 < nb) == 0) break;
+        int key[kBatch];
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) key[k] = min(b0 + k, max(nb - 1, 0));
+        float dot[kBatch];
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) dot[k] = 0.f;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const bf16x8 qv = ld16(qptr[rb] + 16 * c + 8 * half);  // L2-resident
+#pragma unroll
+          for (int k = 0; k < kBatch; ++k) {
+            const bf16x8 kv = lds_ld16(kb0 + (uint32_t)key[k] * kBrPitch + 32u * (uint32_t)c);
+            dot[k] = dot8_bf16(qv, kv, dot[k]);
+          }
+        }
+        float x[kBatch];
+        float m_new = mb;
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+          dot[k] += xor32(dot[k]);
+          x[k] = b0 + k < nb ? dot[k] * p.scale_log2 : -INFINITY;
+          m_new = fmaxf(m_new, x[k]);
+        }
+        if (m_new == -INFINITY) continue;  // no key of this lane's row in the batch
+        const float alpha = fast_exp2(mb - m_new);  // mb = -inf gives 0
+        mb = m_new;
+        lb *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) ob[dt] *= alpha;
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+          const float e = fast_exp2(x[k] - m_new);  // x = -inf gives 0
+          lb += e;
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+            for (int vq = 0; vq < 4; ++vq) {
+              const bf16x4 vv = lds_ld8(vb0 + (uint32_t)key[k] * kBrPitch + 64u * (uint32_t)dt + 16u * (uint32_t)vq);
+#pragma unroll
+              for (int c = 0; c < 4; ++c) ob[dt][4 * vq + c] += e * (float)vv[c];
+            }
+        }
+      }
+    }
+    for (int b = 0; b < (staged ? 0 : BA_MAX_GROUP_LEN); ++b) {
       const bool active = b < nb;
       if (__ballot(active) == 0) break;
       const int64_t krow = (int64_t)gi.row0 + (int64_t)b * gi.stride;
@@ -571,7 +668,7 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
     const float wbr = lse_b == -INFINITY ? 0.f : fast_exp2(lse_b - hi);
     const float tot = wm + wbr;
     const float lse2 = hi + __log2f(tot);
-    const float cm = wm / tot;
+    const float cm = wm / tot * inv;
     const float cb = lb > 0.f ? wbr / (tot * lb) : 0.f;
 
     bf16* out;
@@ -590,8 +687,8 @@ __global__ __launch_bounds__(512 / RB, 1) void fwd_kernel(FwdParams p) {
       for (int vq = 0; vq < 4; ++vq) {
         const int v = 4 * vq;
         *reinterpret_cast<bf16x4*>(out + 32 * dt + 8 * vq + 4 * half) =
-            pack4(cm * st_o[dt][v] + cb * ob[dt][v], cm * st_o[dt][v + 1] + cb * ob[dt][v + 1],
-                  cm * st_o[dt][v + 2] + cb * ob[dt][v + 2], cm * st_o[dt][v + 3] + cb * ob[dt][v + 3]);
+            pack4(cm * o[rb][dt][v] + cb * ob[dt][v], cm * o[rb][dt][v + 1] + cb * ob[dt][v + 1],
+                  cm * o[rb][dt][v + 2] + cb * ob[dt][v + 2], cm * o[rb][dt][v + 3] + cb * ob[dt][v + 3]);
       }
     if (half == 0) *lse_out = lse2 * kLn2;
   };

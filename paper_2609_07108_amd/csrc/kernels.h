@@ -18,6 +18,8 @@ struct FwdParams {
   const GroupInfo* groups;
   const FwdTile* tiles;
   int32_t num_tiles;
+  const int32_t* br_keys;    // branch key rows of the tiles (FwdTile::bk_off)
+  const int32_t* tok_bslot;  // per token: first slot of its group's keys in its tile
   int32_t C, rank, hq, hkv, G;
   int32_t num_tokens;
   float scale_log2;  // softmax scale * log2(e)

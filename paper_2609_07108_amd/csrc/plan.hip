@@ -223,12 +223,42 @@ static int build_plan(const ba_problem* pr, Plan& P) {
     FwdTile t;
   };
   std::vector<Keyed> ft;
+  P.br_keys.clear();
+  P.tok_bslot.assign(P.toks.size(), -1);
   for (int32_t s = 0; s < S; ++s) {
     const SeqInfo& si = P.seqs[s];
     for (int32_t t0 = si.tok_begin; t0 < si.tok_end; t0 += tpt) {
       int32_t n = std::min(tpt, si.tok_end - t0);
       int64_t work = (int64_t)P.toks[t0 + n - 1].P + 1;
-      for (int32_t h = 0; h < pr->hkv; ++h) ft.push_back(Keyed{work, FwdTile{s, t0, n, h}});
+      // the branch-local keys the tile's tokens attend, each group's once:
+      // an EAGLE chain's members 0 .. (deepest member in the tile), a DFlash
+      // block's whole block (shared by every KV head's tile)
+      std::vector<std::pair<int32_t, int32_t>> need;  // (group, keys)
+      for (int32_t t = t0; t < t0 + n; ++t) {
+        const TokInfo& tk = P.toks[t];
+        if (tk.grp < 0) continue;
+        const GroupInfo& g = P.groups[tk.grp];
+        const int32_t k = g.kind == BA_KIND_EAGLE_CHAIN ? tk.gidx + 1 : g.len;
+        auto it = std::find_if(need.begin(), need.end(), [&](const auto& x) { return x.first == tk.grp; });
+        if (it == need.end()) need.emplace_back(tk.grp, k);
+        else it->second = std::max(it->second, k);
+      }
+      int32_t total = 0;
+      for (const auto& x : need) total += x.second;
+      int32_t bk_off = (int32_t)P.br_keys.size(), bk_n = total;
+      if (total > kBrSlots) {
+        bk_n = -1;  // the epilogue reads these keys from global memory
+      } else {
+        int32_t slot = 0;
+        for (const auto& x : need) {
+          const GroupInfo& g = P.groups[x.first];
+          for (int32_t t = t0; t < t0 + n; ++t)
+            if (P.toks[t].grp == x.first) P.tok_bslot[t] = slot;
+          for (int32_t b = 0; b < x.second; ++b) P.br_keys.push_back(g.row0 + b * g.stride);
+          slot += x.second;
+        }
+      }
+      for (int32_t h = 0; h < pr->hkv; ++h) ft.push_back(Keyed{work, FwdTile{s, t0, n, h, bk_off, bk_n}});
     }
   }
   // longest first: the causal prefix length is the tile's work
@@ -336,6 +366,8 @@ void pack_image(Plan& P) {
   P.off_toks = append(P.image, toks_img);
   P.off_groups = append(P.image, P.groups);
   P.off_fwd = append(P.image, P.fwd_tiles);
+  P.off_br_keys = append(P.image, P.br_keys);
+  P.off_bslot = append(P.image, P.tok_bslot);
   P.off_bwd = append(P.image, P.bwd_tiles);
   P.off_splits = append(P.image, P.kv_splits);
   if (P.rope_theta > 0.f) {
