@@ -329,6 +329,8 @@ extern "C" int branch_attn_bwd(void* stream_, const ba_plan* plan, int32_t mode,
   const BwdTile* tiles = reinterpret_cast<const BwdTile*>(c.ws + c.w.tables + P.off_bwd);
   p.qtiles = reinterpret_cast<const FwdTile*>(c.ws + c.w.tables + P.off_fwd);
   p.num_qtiles = (int32_t)P.fwd_tiles.size();
+  p.br_keys = reinterpret_cast<const int32_t*>(c.ws + c.w.tables + P.off_br_keys);
+  p.tok_bslot = reinterpret_cast<const int32_t*>(c.ws + c.w.tables + P.off_bslot);
   p.C = P.cp_size;
   p.rank = P.cp_rank;
   p.hq = P.hq;

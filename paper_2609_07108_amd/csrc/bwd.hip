@@ -21,8 +21,9 @@
 //                64 rows per wavefront): per key tile S^T = K Q^T,
 //                dP^T = V dO^T, dS^T, dQ^T += K^T dS^T, software-pipelined
 //                across key tiles; the branch-local keys' terms are the
-//                accumulators' start value in the fused schedule and are
-//                added by the finalize kernel in the per-step one.
+//                accumulators' start value in the fused schedule (from the
+//                tile's branch keys staged once in LDS) and are added by the
+//                finalize kernel in the per-step one.
 //                Splitting dQ off
 //                costs two extra contractions but avoids fp32 atomics, whose
 //                throughput (about one 4-byte update per L2 channel and clock)
@@ -659,6 +660,10 @@ __global__ __launch_bounds__(256) void bwd_kv_reduce_kernel(BwdParams p) {
 namespace {
 
 constexpr int kDqBufs = 3;
+// FUSED: a query tile's branch-local keys staged in LDS next to the K/V
+// buffers for the branch terms (K rows then V rows, kBrPitch apart); a tile
+// with more keys computes them from global memory
+constexpr int kDqBrSlots = 120;
 constexpr int kDqAhead = 3;  // operand fragments read ahead of their MFMAs (two MFMAs each)
 
 // Element e of a key block (32 per lane): the 8-key chunk tt = e/16 (keys
@@ -677,6 +682,7 @@ template <int MODE>
 __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
   // [buffer][K, V] plane tiles of 64 keys (see tile_off)
   __shared__ __attribute__((aligned(16))) bf16 kvbuf[kDqBufs][2][kFwdKeys * kHeadDim];
+  __shared__ __attribute__((aligned(16))) unsigned char brbuf[MODE == kModeFused ? 2 * kDqBrSlots * kBrPitch : 16];
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
   const FwdTile tile = p.qtiles[blockIdx.x];
@@ -754,20 +760,53 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
   // dS K with P and dS from the row statistics as for a main key.  The
   // scores take the register-held Q and dO (dims 16 c + 8 half + 0..7) and
   // K, V read in that layout; dS K takes K again in the accumulator layout
-  // (dims 32 dt + 8 vq + 4 half + 0..3), all of a key in one round trip to
-  // memory.  A lane past its keys (or without any) reloads a valid row and
-  // gives it weight 0.
+  // (dims 32 dt + 8 vq + 4 half + 0..3).  The keys come from the tile's
+  // staged copy in LDS (the planner's list, each group's keys once); a tile
+  // with more than kDqBrSlots keys reads each key's rows from global memory,
+  // in one round trip per key.  A lane past its keys (or without any) reads
+  // a valid key and gives it weight 0.
+  const bool staged = MODE == kModeFused && tile.bk_n > 0 && tile.bk_n <= kDqBrSlots;
+  const uint32_t br_lds = lds_addr(&brbuf[0]);
   auto seed_branch = [&](int rb) {
     int nb = 0;
+    int bslot = 0;
     GroupInfo gi{0, 1, 0, 0, 0, 0, {0, 0}};
     if (valid[rb] && tk[rb].grp >= 0) {
       gi = p.groups[tk[rb].grp];
       nb = gi.kind == BA_KIND_EAGLE_CHAIN ? tk[rb].gidx + 1 : gi.len;
+      if (staged) bslot = p.tok_bslot[tile.tok_begin + (64 * wave + 32 * rb + qi) / p.G];
     }
     f32x16 acc[4];
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x16{};
-    if (__ballot(nb > 0)) {
+    if (staged && __ballot(nb > 0)) {
+      // the staged keys: LDS reads per key instead of a global round trip
+      const uint32_t k0 = br_lds + (uint32_t)bslot * kBrPitch;
+      const uint32_t v0 = k0 + (uint32_t)(kDqBrSlots * kBrPitch);
+      for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
+        if (__ballot(b < nb) == 0) break;
+        const uint32_t ko = k0 + (uint32_t)min(b, max(nb - 1, 0)) * kBrPitch;
+        const uint32_t vo = v0 + (uint32_t)min(b, max(nb - 1, 0)) * kBrPitch;
+        float sdot = 0.f, pdot = 0.f;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          sdot = dot8_bf16(qreg[rb][c], lds_ld16(ko + 32u * c + 16u * half), sdot);
+          pdot = dot8_bf16(greg[rb][c], lds_ld16(vo + 32u * c + 16u * half), pdot);
+        }
+        sdot += xor32(sdot);
+        pdot += xor32(pdot);
+        const float pr = b < nb ? fast_exp2(sdot * p.scale_log2 + nl2[rb]) : 0.f;
+        const float ds = pr * (pdot + ndl[rb]);
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int vq = 0; vq < 4; ++vq) {
+            const bf16x4 kk = lds_ld8(ko + 64u * dt + 16u * vq + 8u * half);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) acc[dt][4 * vq + c] += ds * (float)kk[c];
+          }
+      }
+    } else if (__ballot(nb > 0)) {
       for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
         if (__ballot(b < nb) == 0) break;
         const int bu = min(b, max(nb - 1, 0));
@@ -1004,6 +1043,34 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
     };
 
     KvCursor cur = seek(p.step_first);
+    if (staged) {
+      // the tile's branch keys into LDS (before the first tile's direct
+      // loads, which the waits for these loads would otherwise cover too)
+      constexpr int kUnroll = 4;
+      const int nch = tile.bk_n * 32;  // 16-byte chunks: 16 of K and 16 of V per key
+      for (int c0 = tid; c0 < nch; c0 += kUnroll * 256) {
+        int32_t krow[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) krow[u] = p.br_keys[tile.bk_off + (min(c0 + u * 256, nch - 1) >> 5)];
+        bf16x8 v[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const int part = min(c0 + u * 256, nch - 1) & 31;
+          v[u] = ld16((part < 16 ? p.k_br : p.v_br) + (int64_t)krow[u] * kv_row_stride + tile.kvh * kHeadDim +
+                      8 * (part & 15));
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const int c = c0 + u * 256;
+          const int part = c & 31;
+          if (c < nch)
+            lds_st16(br_lds + (part < 16 ? 0u : (uint32_t)(kDqBrSlots * kBrPitch)) + (uint32_t)(c >> 5) * kBrPitch +
+                         16u * (uint32_t)(part & 15),
+                     v[u]);
+        }
+      }
+      __syncthreads();
+    }
     if (cur.i < step_end) {
       const DmaTile d0 = dma_tile(cur, 0);
 #pragma unroll

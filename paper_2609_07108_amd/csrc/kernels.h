@@ -48,6 +48,8 @@ struct BwdParams {
   int32_t num_tiles;
   const FwdTile* qtiles;  // query tiles of the dQ kernel
   int32_t num_qtiles;
+  const int32_t* br_keys;    // branch key rows of the query tiles (FwdTile::bk_off)
+  const int32_t* tok_bslot;  // per token: first slot of its group's keys in its tile
   int32_t step_first, step_count, acc_first;
   int32_t C, rank, hq, hkv, G;
   int32_t num_tokens;
