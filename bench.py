@@ -37,9 +37,9 @@ PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/c
 # calibration (profiles/traffic_eagle3-K3-L262144-cp8r0.md).  A figure only
 # applies while the kernel's source is the one that was measured.
 MEASURED_TRAFFIC = {
-    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "1201376888cec409", "bytes": 14589234050},
-    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "1201376888cec409", "bytes": 7797859904},
-    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "a3b88d8a6e57f733", "bytes": 7168329394},
+    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "92053948b1692c97", "bytes": 15304893928},
+    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "92053948b1692c97", "bytes": 7807579430},
+    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 7168862288},
 }
 
 def measured_traffic(kernel: str, workload: str, mode: str):
