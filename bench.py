@@ -33,10 +33,14 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/clk x 2.4 GHz
 
 # HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE runs of
-# this benchmark (256K headline share, per-step schedule), scaled by a plain-copy
-# calibration (profiles/traffic_eagle3-K3-L262144-cp8r0.md).  A figure only
-# applies while the kernel's source is the one that was measured.
+# this benchmark (256K headline share; the fused schedule, the plan's choice,
+# in profiles/traffic_eagle3-K3-L262144-cp8r0.md, and the per-step schedule
+# taken on the same sources), scaled by a plain-copy calibration.  A figure
+# only applies while the kernel's source is the one that was measured.
 MEASURED_TRAFFIC = {
+    ("bwd_kv_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "92053948b1692c97", "bytes": 15346021694},
+    ("bwd_dq_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "92053948b1692c97", "bytes": 38220175220},
+    ("fwd_kernel", "fused"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 37982062549},
     ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "92053948b1692c97", "bytes": 15304893928},
     ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "92053948b1692c97", "bytes": 7807579430},
     ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 7168862288},
@@ -293,7 +297,7 @@ def main():
     ap.add_argument("--config", type=int, default=4, help="named workload 1..5 (4 = 256K headline)")
     ap.add_argument("--mode", choices=["auto", "fused", "per_step"], default="auto",
                     help="per_step: one launch per ring step (the ring's schedule); fused: one walk over all "
-                         "blocks; auto (default): the plan's choice (per-step at the 256K share)")
+                         "blocks; auto (default): the plan's choice (fused)")
     ap.add_argument("--cpu-rows", type=int, default=48,
                     help="query rows of the CPU oracle sample (about 12 s on 16 cores; 0 disables)")
     ap.add_argument("--rope", type=float, default=0.0, metavar="THETA",
@@ -391,8 +395,8 @@ def main():
     fwd_ring_ms = sum(ev.ms(a, b) for a, b in zip(fb, fe)) / args.steps
     bwd_ring_ms = sum(ev.ms(a, b) for a, b in zip(bb, be)) / args.steps
     # the backward ring part is two kernels: dK/dV (S, dP, dV, dK: 8d per
-    # pair) then dQ (S, dP, dQ: 6d per pair); in the per-step schedule each
-    # is C launches, so time per launch and FLOPs per launch scale alike
+    # pair) then dQ (S, dP, dQ: 6d per pair); a kernel's time and FLOPs are
+    # summed over its launches of the call, so their ratio is per launch too
     kv_ms = sum(ev.ms(a, b) for a, b in zip(bb, bk)) / args.steps
     kern = {"fwd_kernel": (fwd_ring_ms, ring_fwd_flops),
             "bwd_kv_kernel": (kv_ms, main_pairs * hq * 8 * d),
@@ -401,8 +405,12 @@ def main():
           ", ".join(f"{k} {v[0]:.2f} ms ({v[1] / v[0] / 1e9:.0f} TFLOP/s)" for k, v in kern.items()),
           file=sys.stderr, flush=True)
 
-    launches = 1 if mode == B.BA_MODE_FUSED else prob.cp_size
+    # launches per call: dK/dV once per ring step in both schedules, the
+    # forward and dQ once (fused) or once per ring step
+    per_call = 1 if mode == B.BA_MODE_FUSED else prob.cp_size
+    launches_of = {"fwd_kernel": per_call, "bwd_kv_kernel": prob.cp_size, "bwd_dq_kernel": per_call}
     dom_name = max(kern, key=lambda k: kern[k][0])
+    launches = launches_of[dom_name]
     dom_ms, dom_flops = kern[dom_name]
     achieved = dom_flops / (dom_ms / 1e3) / 1e12
     value = (f_fwd + f_bwd) / (ms_step / 1e3) / 1e12
@@ -424,7 +432,7 @@ def main():
     alg_bwd = nq * (row_q * 4 + hq * 4) + n_kv * row_kv * 4
     alg_bytes = alg_fwd + alg_bwd
     meas = [measured_traffic(k, prob.name, mode_name) for k in kern] if not args.rope else [None]
-    meas_bytes = sum(m * launches for m in meas) if all(m is not None for m in meas) else None
+    meas_bytes = sum(m * launches_of[k] for k, m in zip(kern, meas)) if all(m is not None for m in meas) else None
 
     n_local, ntok = share.plan.info()
     traffic = measured_traffic(dom_name, prob.name, mode_name) if not args.rope else None

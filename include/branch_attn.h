@@ -68,11 +68,11 @@ extern "C" {
  * once per ring step. */
 #define BA_MODE_PER_STEP 0
 #define BA_MODE_FUSED 1
-/* BA_MODE_AUTO: the plan picks one of the two.  Per-step when every ring
- * step's dK/dV launch has enough work items to fill the GPU on its own (1024
- * before any splitting); fused otherwise (shares of short sequences), where
- * per-step launches leave the GPU partly idle and pay a running-sum pass per
- * step.  Accepted wherever a mode is. */
+/* BA_MODE_AUTO: the plan picks one of the two; today the fused schedule for
+ * every plan, measured the faster one on one GPU for every share (the
+ * per-step schedule pays a running-sum pass per ring step and finalize
+ * passes; both launch dK/dV per ring step).  branch_attn_plan_mode reports
+ * the choice.  Accepted wherever a mode is. */
 #define BA_MODE_AUTO 2
 
 #define BA_MAX_GROUP_LEN 64    /* members per branch group                 */

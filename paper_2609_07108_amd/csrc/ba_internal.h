@@ -203,9 +203,7 @@ struct Plan {
   double pairs_per_head = 0.0;  // allowed (query, key) pairs per query head
   double main_pairs_per_head = 0.0;   // ... of which on the causal main prefix
   int32_t max_group_len = 0;
-  // schedule BA_MODE_AUTO resolves to: per-step when every ring step's dK/dV
-  // launch has at least kKvSplitBelow work items before splitting (the
-  // launches fill the GPU), fused otherwise
+  // schedule BA_MODE_AUTO resolves to (fused; see build_plan)
   int32_t auto_mode = 1;
 };
 

@@ -270,7 +270,6 @@ static int build_plan(const ba_problem* pr, Plan& P) {
   // step in the order the ring delivers the blocks (step i brings rank
   // (r - i) mod C), longest first inside a step
   P.bwd_step_off.assign(C + 1, 0);
-  int32_t min_items = INT32_MAX;  // work items of the emptiest non-empty ring step, before splitting
   for (int32_t i = 0; i < C; ++i) {
     const int32_t j = ((r - i) % C + C) % C;
     struct KeyedB {
@@ -300,7 +299,6 @@ static int build_plan(const ba_problem* pr, Plan& P) {
                               BwdTile{j, s, h, u0, nk, qb, qf, si.tok_end, -1, 0, {0, 0}}});
       }
     }
-    if (!bt.empty()) min_items = std::min(min_items, (int32_t)bt.size());
     // few items: split the longest along their query range (whole 64-row
     // query tiles per piece) into pieces of about total / kKvSplitBelow
     if (!bt.empty() && (int32_t)bt.size() < kKvSplitBelow) {
@@ -345,12 +343,12 @@ static int build_plan(const ba_problem* pr, Plan& P) {
     for (auto& k : bt) P.bwd_tiles.push_back(k.t);
     P.bwd_step_off[i + 1] = (int32_t)P.bwd_tiles.size();
   }
-  // per-step launches pay a running-sum pass per ring step; they are worth it
-  // only when every step alone fills the GPU (measured: the 256K share and
-  // the 32K DFlash sequence, 2048 items per step, per-step 1.4 % and 4 %
-  // faster; 8 varlen sequences at CP = 4 and 16 at CP = 8, fewer items per
-  // step, fused 2.5 % and 17 % faster)
-  P.auto_mode = (min_items != INT32_MAX && min_items >= kKvSplitBelow) ? BA_MODE_PER_STEP : BA_MODE_FUSED;
+  // the fused schedule: with dK/dV launched per ring step in both schedules
+  // and the branch-local keys staged in LDS, it is the faster one on every
+  // measured share (the forward and dQ skip the per-step running sums and
+  // their finalize passes): 256K share -0.7 %, 32K DFlash sequence -0.9 %,
+  // shares of short sequences more
+  P.auto_mode = BA_MODE_FUSED;
 
   pack_image(P);
   return BA_OK;

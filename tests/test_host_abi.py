@@ -191,10 +191,9 @@ def test_device_calls_reject_more_than_32_ring_steps():
 
 
 def test_auto_schedule_choice_per_plan():
-    """BA_MODE_AUTO: per-step only when every ring step's dK/dV launch fills
-    the GPU on its own (the 256K share, the 32K DFlash sequence); fused for
-    the shares of short sequences."""
-    want = {2: B.BA_MODE_FUSED, 3: B.BA_MODE_PER_STEP, 4: B.BA_MODE_PER_STEP, 5: B.BA_MODE_FUSED}
+    """BA_MODE_AUTO resolves to the fused schedule, measured the faster one
+    on every workload; the explicit modes resolve to themselves."""
+    want = {2: B.BA_MODE_FUSED, 3: B.BA_MODE_FUSED, 4: B.BA_MODE_FUSED, 5: B.BA_MODE_FUSED}
     for cfg, mode in want.items():
         share = RS.build_share(W.config(cfg), materialize=False)
         assert share.plan.mode(B.BA_MODE_AUTO) == mode, cfg
