@@ -67,6 +67,14 @@ def case(name):
         # rank (its two chunks are the middle of each sequence)
         return W.custom([2048, 1024], [("eagle", 2), ("dflash", 8, 32)], hq=4, hkv=4, cp_size=32, cp_rank=31,
                         seed=211, name=name)
+    if name == "branch_key_limits":
+        # one KV head per query head, so a query tile holds 256 tokens: the
+        # depth-64 chains put up to 315 distinct branch keys into a tile
+        # (more than the fused forward stages in LDS: its rows read them
+        # from global memory), most tiles more than the fused dQ stages, a
+        # DFlash tile few enough for both
+        return W.custom([384, 96], [("eagle", 64), ("dflash", 32, 64, 2)], hq=2, hkv=2, cp_size=2, cp_rank=1,
+                        seed=212, anchor_seed=31, name=name)
     raise KeyError(name)
 
 
@@ -101,6 +109,7 @@ def test_config1_forward_every_rank(cuda, mode, r):
     ("gqa_g64", "depth", torch.float32),
     ("cp16", "group", torch.bfloat16),
     ("cp32_max", "depth", torch.float32),
+    ("branch_key_limits", "group", torch.bfloat16),
 ])
 def test_forward_backward_parity(cuda, mode, name, layout, grad_dtype):
     prob = case(name)
