@@ -241,7 +241,8 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   const uint32_t g_lds = lds_addr(&sm.gs[0]);
   // Q of the tile at stage position kq (score wavefronts) or dO of the one
   // at position kg (gradient wavefronts); past the last position its tile
-  // again, into the position's own (idle) buffer.  A stage's loads go out in 9 pieces spread over its schedule:
+  // again, into the position's own (idle) buffer.  A stage's loads go out in 9 pieces in its first slots (the
+  // buffers they fill, those of tile s-1, are free from the stage's start):
   // pieces 0-7 are the row loads (rows 32 pair + 16 (piece/4) + lane/4,
   // plane piece%4), piece 8 the statistic.
   const bf16* rows_src = scorer ? p.qtok : p.gtok;
@@ -437,7 +438,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
         }
         if constexpr (active) mfma(j, opq[f % (kOpAhead + 1)]);
         if constexpr (j == 2) dma_piece(dm, 8);
-        if constexpr ((j & 7) == 4) dma_piece(dm, j >> 3);
+        if constexpr (j >= 3 && j < 11) dma_piece(dm, j - 3);
         __builtin_amdgcn_sched_barrier(0);
       });
     };
@@ -558,7 +559,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
         });
         mfma(j, opq[f % (kOpAhead + 1)]);
         if constexpr (j == 2) dma_piece(dm, 8);
-        if constexpr ((j & 7) == 4) dma_piece(dm, j >> 3);
+        if constexpr (j >= 3 && j < 11) dma_piece(dm, j - 3);
         __builtin_amdgcn_sched_barrier(0);
       });
     };
