@@ -91,28 +91,31 @@ __device__ __forceinline__ bf16x8 tr_frag(const OpBases& o, int t, int nt) {
 }  // namespace
 
 // ------------------------------------------------------------ preprocess
-// 32 lanes per (token, head): -Delta = -<dO, O> over 128 dims and -LSE in
-// log2 units (both stored negated so the dK/dV kernel can start its S and dP
-// accumulations from them); Q and dO rows are also copied into token order, so the
-// dK/dV kernel addresses a query tile without indirection.
+// 16 lanes (a DPP row) per (token, head), 16 bytes each: -Delta = -<dO, O>
+// over 128 dims and -LSE in log2 units (both stored negated so the dK/dV
+// kernel can start its S and dP accumulations from them); Q and dO rows are
+// also copied into token order, so the dK/dV kernel addresses a query tile
+// without indirection.  Rows past the end redo the last row and write
+// nothing (the DPP row sum needs every lane).
 __global__ __launch_bounds__(256) void bwd_preprocess_kernel(BwdParams p) {
-  const int64_t pair = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 5;
-  const int sub = threadIdx.x & 31;
-  if (pair >= (int64_t)p.num_tokens * p.hq) return;
+  const int64_t rows = (int64_t)p.num_tokens * p.hq;
+  const int64_t pair0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
+  const bool live = pair0 < rows;
+  const int64_t pair = live ? pair0 : rows - 1;
+  const int sub = threadIdx.x & 15;
   const int32_t t = (int32_t)(pair / p.hq);
   const int32_t head = (int32_t)(pair - (int64_t)t * p.hq);
   const TokInfo tk = p.toks[t];
-  const bf16* o = row_ptr(p.o_main, p.o_br, tk.qrow, p.hq, head);
-  const bf16* g = row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head);
-  const bf16x4 ov = reinterpret_cast<const bf16x4*>(o)[sub];
-  const bf16x4 gv = reinterpret_cast<const bf16x4*>(g)[sub];
-  const bf16x4 qv = reinterpret_cast<const bf16x4*>(row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head))[sub];
-  reinterpret_cast<bf16x4*>(p.qtok + pair * kHeadDim)[sub] = qv;
-  reinterpret_cast<bf16x4*>(p.gtok + pair * kHeadDim)[sub] = gv;
-  float dlt = (float)ov[0] * (float)gv[0] + (float)ov[1] * (float)gv[1] + (float)ov[2] * (float)gv[2] +
-              (float)ov[3] * (float)gv[3];
+  const bf16x8 ov = ld16(row_ptr(p.o_main, p.o_br, tk.qrow, p.hq, head) + 8 * sub);
+  const bf16x8 gv = ld16(row_ptr(p.do_main, p.do_br, tk.qrow, p.hq, head) + 8 * sub);
+  const bf16x8 qv = ld16(row_ptr(p.q_main, p.q_br, tk.qrow, p.hq, head) + 8 * sub);
+  float dlt = 0.f;
 #pragma unroll
-  for (int m = 16; m >= 1; m >>= 1) dlt += __shfl_xor(dlt, m, 32);
+  for (int e = 0; e < 8; ++e) dlt += (float)ov[e] * (float)gv[e];
+  dlt = row16_sum(dlt);
+  if (!live) return;
+  st16(p.qtok + pair * kHeadDim + 8 * sub, qv);
+  st16(p.gtok + pair * kHeadDim + 8 * sub, gv);
   if (sub == 0) {
     const float lse = tk.qrow >= 0 ? p.lse_main[(int64_t)head * p.n_local + tk.qrow]
                                    : p.lse_br[(int64_t)head * p.n_br + (-tk.qrow - 1)];
@@ -1371,7 +1374,7 @@ static unsigned grid_for(int64_t threads) {
 }
 
 hipError_t launch_bwd_preprocess(const BwdParams& p, hipStream_t stream) {
-  const int64_t threads = (int64_t)p.num_tokens * p.hq * 32;
+  const int64_t threads = (int64_t)p.num_tokens * p.hq * 16;
   if (threads == 0) return hipSuccess;
   hipLaunchKernelGGL(bwd_preprocess_kernel, dim3(grid_for(threads)), dim3(256), 0, stream, p);
   return hipGetLastError();
