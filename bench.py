@@ -38,12 +38,12 @@ PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/c
 # taken on the same sources), scaled by a plain-copy calibration.  A figure
 # only applies while the kernel's source is the one that was measured.
 MEASURED_TRAFFIC = {
-    ("bwd_kv_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "bd03b562c3bded1e", "bytes": 9965470502},
-    ("bwd_dq_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "bd03b562c3bded1e", "bytes": 38219705461},
-    ("fwd_kernel", "fused"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 37983064389},
-    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "bd03b562c3bded1e", "bytes": 9974326053},
-    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "bd03b562c3bded1e", "bytes": 7800133454},
-    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 7169362406},
+    ("bwd_kv_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "d63af6d1c91449cb", "bytes": 9967392681},
+    ("bwd_dq_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "d63af6d1c91449cb", "bytes": 38220095143},
+    ("fwd_kernel", "fused"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 37981459423},
+    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "d63af6d1c91449cb", "bytes": 9949089343},
+    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "d63af6d1c91449cb", "bytes": 7800042508},
+    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 7167971964},
 }
 
 def measured_traffic(kernel: str, workload: str, mode: str):
