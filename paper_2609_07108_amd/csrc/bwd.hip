@@ -961,9 +961,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
 
     // One tile iteration.  MFMA j (0..95): phase j/16; fragment j/2 feeds
     // MFMAs j (row block 0) and j+1 (row block 1).  The current tile is in
-    // buffer cb, the previous one in pb; mask: apply the causal limits.
-    auto iterate = [&](auto tail_tag, int cb, int pb, const KvCursor& cur, bool mask, const DmaTile& dn,
-                       bool load_next) __attribute__((always_inline)) {
+    // buffer cb, the previous one in pb; mask: apply the causal limits; dn:
+    // the tile loaded into the third buffer.
+    auto iterate = [&](auto tail_tag, int cb, int pb, const KvCursor& cur, bool mask,
+                       const DmaTile& dn) __attribute__((always_inline)) {
       constexpr bool TAIL = decltype(tail_tag)::value;  // phase 1 and key block 1 of the previous tile only
       const bf16* kc = &kvbuf[cb][0][0];
       const bf16* vc = &kvbuf[cb][1][0];
@@ -1037,9 +1038,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
           });
           // direct loads of tile t+1, in the first slots: its buffer (tile
           // t-2's) is free from the iteration's start
-          if constexpr (j < 8) {
-            if (load_next) fetch_piece(dn, j);
-          }
+          if constexpr (j < 8) fetch_piece(dn, j);
         }
         if constexpr (act) mfma(j, opq[f % (kDqAhead + 1)]);
         __builtin_amdgcn_sched_barrier(0);
@@ -1101,10 +1100,12 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
       while (true) {
         const KvCursor nx = next(cur);
         const bool more = nx.i < step_end;
+        // with no tile t+1 the loads repeat tile t into the idle buffer
+        // (unconditional loads: no branch between the first MFMA slots)
         const DmaTile dn = dma_tile(more ? nx : cur, (t + 1) % kDqBufs);
         const bool mask = cur.kv0 + kFwdKeys > cur.lim_lo;
         // the first tile's stand-in previous tile reads this tile's (finite) K
-        iterate(std::false_type{}, t % kDqBufs, t == 0 ? 0 : (t - 1) % kDqBufs, cur, mask, dn, more);
+        iterate(std::false_type{}, t % kDqBufs, t == 0 ? 0 : (t - 1) % kDqBufs, cur, mask, dn);
         wait_vmcnt_lgkm0<0>();  // tile t+1 has landed for this wavefront
         lds_barrier();
         ++t;
@@ -1112,7 +1113,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
         cur = nx;
       }
       // key block 1 of the last tile
-      iterate(std::true_type{}, 0, (t - 1) % kDqBufs, cur, false, DmaTile{}, false);
+      iterate(std::true_type{}, 0, (t - 1) % kDqBufs, cur, false, DmaTile{});
       mfma_drain();  // dQ^T complete before the epilogue reads it
     }
   }
