@@ -229,7 +229,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
 
   // ---- direct loads: the score wavefronts load Q rows 32 w + 16 j + lane/4
   // (j = 0, 1), the gradient wavefronts the same rows of dO; wavefront 0
-  // also loads the tile's LSE, 1 its causal limits, 2 its -Delta.  Rows
+  // also loads the tile's LSE, 1 its causal limits, 2 and 3 its -Delta.  Rows
   // without a token read the tile's first row (finite data) and the
   // sentinel token's limit -1.
   int dtl[2], dhg[2];
@@ -267,17 +267,22 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   };
   auto dma_piece = [&](const DmaStage& d, int piece) __attribute__((always_inline)) {
     if (piece == 8) {
+      // one statistic per wavefront, chosen by wavefront-uniform selects
+      // (no branch between the first MFMA slots); wavefront 3 repeats
+      // wavefront 2's load (the same words into the same LDS buffer), so
+      // every wavefront has nine loads per stage
       const bool ok = stl < tpt && stl < d.nt;
-      if (wave == 1) {
-        const void* base = uniform_ptr(p.toks + d.qt0);
-        const uint32_t off = (uint32_t)((ok ? stl : p.num_tokens - d.qt0) * (int)sizeof(TokInfo) +
-                                        (int)offsetof(TokInfo, P));
-        dma4_async(base, off, d.b + (uint32_t)offsetof(QSide, pl));
-      } else if (wave != 3) {
-        const void* base = uniform_ptr(p.rowstat + (int64_t)d.qt0 * p.hq + head0);
-        const uint32_t off = (uint32_t)((ok ? stl * p.hq + shg : 0) * (int)sizeof(float2) + (wave == 0 ? 0 : 4));
-        dma4_async(base, off, d.b + (uint32_t)(wave == 0 ? offsetof(QSide, l2) : offsetof(GSide, nd)));
-      }
+      const bool limits = wave == 1;
+      const void* b_lim = uniform_ptr(p.toks + d.qt0);
+      const void* b_stat = uniform_ptr(p.rowstat + (int64_t)d.qt0 * p.hq + head0);
+      asm volatile("" : "+s"(b_lim), "+s"(b_stat));  // both computed: a select, not a branch
+      const void* base = limits ? b_lim : b_stat;
+      const int off_lim = (ok ? stl : p.num_tokens - d.qt0) * (int)sizeof(TokInfo) + (int)offsetof(TokInfo, P);
+      const int off_stat = (ok ? stl * p.hq + shg : 0) * (int)sizeof(float2) + (wave == 0 ? 0 : 4);
+      const uint32_t dst = wave == 0 ? (uint32_t)offsetof(QSide, l2)
+                           : limits  ? (uint32_t)offsetof(QSide, pl)
+                                     : (uint32_t)offsetof(GSide, nd);
+      dma4_async(base, (uint32_t)(limits ? off_lim : off_stat), d.b + dst);
       return;
     }
     const int j = piece >> 2, pl = piece & 3;
@@ -295,11 +300,10 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(BwdParams p) {
   };
   // End of a stage: this wavefront's loads issued before the stage (the
   // tiles the next stage reads) have landed and its P writes are done; the
-  // loads of this stage (9 for wavefronts 0-2, 8 for wavefront 3) stay in
-  // flight.  The barrier publishes everything to the workgroup.
+  // nine loads of this stage stay in flight.  The barrier publishes
+  // everything to the workgroup.
   auto stage_end = [&]() __attribute__((always_inline)) {
-    if (wave == 3) wait_vmcnt_lgkm0<8>();
-    else wait_vmcnt_lgkm0<9>();
+    wait_vmcnt_lgkm0<9>();
     lds_barrier();
   };
 
