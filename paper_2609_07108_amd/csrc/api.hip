@@ -78,7 +78,8 @@ struct RopeTables {
   const int32_t* pos_block;  // [C][n_local]
   const int32_t* pos_qmain;  // [n_local]
   const int32_t* pos_br;     // [num_branch_rows]
-  const RopeFreq* freq;
+  const RopeFreq* freq;      // turns per position (float pair), gradient rotation
+  const double* rad;         // radians per position (double), input rotation
 };
 
 RopeTables rope_tables(const Plan& P, const Common& c) {
@@ -86,7 +87,8 @@ RopeTables rope_tables(const Plan& P, const Common& c) {
   return RopeTables{reinterpret_cast<const int32_t*>(t + P.off_pos_block),
                     reinterpret_cast<const int32_t*>(t + P.off_pos_qmain),
                     reinterpret_cast<const int32_t*>(t + P.off_pos_br),
-                    reinterpret_cast<const RopeFreq*>(t + P.off_freq)};
+                    reinterpret_cast<const RopeFreq*>(t + P.off_freq),
+                    reinterpret_cast<const double*>(t + P.off_rad)};
 }
 
 // Rotated bf16 copies of the queries and keys of one call; the pointers the
@@ -101,21 +103,21 @@ hipError_t rotate_inputs(const Plan& P, const Common& c, const void* q_main, con
   hipError_t e = hipSuccess;
   if (has_main) {
     bf16* rq = reinterpret_cast<bf16*>(c.ws + c.w.rq_main);
-    if ((e = launch_rope_rows(static_cast<const bf16*>(q_main), rq, rt.pos_qmain, rt.freq, nl, P.hq, stream)))
+    if ((e = launch_rope_rows(static_cast<const bf16*>(q_main), rq, rt.pos_qmain, rt.rad, nl, P.hq, stream)))
       return e;
     p.q_main = rq;
   }
   if (has_br) {
     bf16* rq = reinterpret_cast<bf16*>(c.ws + c.w.rq_br);
     bf16* rk = reinterpret_cast<bf16*>(c.ws + c.w.rk_br);
-    if ((e = launch_rope_rows(static_cast<const bf16*>(q_br), rq, rt.pos_br, rt.freq, nb, P.hq, stream))) return e;
-    if ((e = launch_rope_rows(static_cast<const bf16*>(k_br), rk, rt.pos_br, rt.freq, nb, P.hkv, stream))) return e;
+    if ((e = launch_rope_rows(static_cast<const bf16*>(q_br), rq, rt.pos_br, rt.rad, nb, P.hq, stream))) return e;
+    if ((e = launch_rope_rows(static_cast<const bf16*>(k_br), rk, rt.pos_br, rt.rad, nb, P.hkv, stream))) return e;
     p.q_br = rq;
     p.k_br = rk;
   }
   for (int j = 0; j < P.cp_size && has_keys; ++j) {
     bf16* rk = reinterpret_cast<bf16*>(c.ws + c.w.rk_step) + (int64_t)j * nl * krow;
-    if ((e = launch_rope_rows(static_cast<const bf16*>(k_step[j]), rk, rt.pos_block + (int64_t)j * nl, rt.freq, nl,
+    if ((e = launch_rope_rows(static_cast<const bf16*>(k_step[j]), rk, rt.pos_block + (int64_t)j * nl, rt.rad, nl,
                               P.hkv, stream)))
       return e;
     p.k_step[j] = rk;

@@ -65,6 +65,10 @@ struct RopeFreq {
 
 // The 64 frequencies of base theta (> 0), computed in double and split.
 void rope_freq_table(float theta, RopeFreq* out);
+// The same 64 frequencies in radians per position, theta^(-j/64), in double:
+// the rotation of the attention's inputs takes its angles, sine, cosine and
+// products in double and rounds once to bf16.
+void rope_rad_table(float theta, double* out);
 
 // sin and cos of the angle of dim pair f at position pos.  The turns
 // pos * f are formed as an unevaluated float sum, the product's rounding
@@ -198,7 +202,8 @@ struct Plan {
   std::vector<int32_t> pos_qmain;
   std::vector<int32_t> pos_br;
   std::vector<RopeFreq> rope_freq;
-  size_t off_pos_block = 0, off_pos_qmain = 0, off_pos_br = 0, off_freq = 0;
+  std::vector<double> rope_rad;
+  size_t off_pos_block = 0, off_pos_qmain = 0, off_pos_br = 0, off_freq = 0, off_rad = 0;
   // counts
   double pairs_per_head = 0.0;  // allowed (query, key) pairs per query head
   double main_pairs_per_head = 0.0;   // ... of which on the causal main prefix

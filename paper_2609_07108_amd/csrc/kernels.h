@@ -102,8 +102,9 @@ hipError_t launch_bwd_dq_finalize(const BwdParams& p, hipStream_t stream);
 hipError_t launch_bwd_branch(const BwdParams& p, int max_group_len, hipStream_t stream);
 hipError_t launch_bwd_kv_reduce(const BwdParams& p, hipStream_t stream);
 hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t stream);
-// rotary embedding of bf16 rows [rows, heads, 128] (positions < 0: row skipped)
-hipError_t launch_rope_rows(const bf16* src, bf16* dst, const int32_t* pos, const RopeFreq* freq, int64_t rows,
+// rotary embedding of bf16 rows [rows, heads, 128] (positions < 0: row
+// skipped), evaluated in double from the radian table and rounded once
+hipError_t launch_rope_rows(const bf16* src, bf16* dst, const int32_t* pos, const double* rad, int64_t rows,
                             int heads, hipStream_t stream);
 // transposed rotation (or, with rotate false, a plain copy) of fp32 gradient
 // rows into bf16 or fp32 rows

@@ -373,6 +373,7 @@ void pack_image(Plan& P) {
     P.off_pos_qmain = append(P.image, P.pos_qmain);
     P.off_pos_br = append(P.image, P.pos_br);
     P.off_freq = append(P.image, P.rope_freq);
+    P.off_rad = append(P.image, P.rope_rad);
   }
   P.image.resize((P.image.size() + 255) & ~size_t(255));
 }
@@ -390,6 +391,10 @@ void rope_freq_table(float theta, RopeFreq* out) {
   }
 }
 
+void rope_rad_table(float theta, double* out) {
+  for (int j = 0; j < kHeadDim / 2; ++j) out[j] = std::pow((double)theta, -(double)j / (kHeadDim / 2));
+}
+
 static int build_rope(Plan& P, float theta) {
   if (!std::isfinite(theta) || theta < 0.f) return fail(BA_E_INVAL, "rope theta must be finite and >= 0");
   P.rope_theta = theta;
@@ -397,6 +402,7 @@ static int build_rope(Plan& P, float theta) {
   P.pos_qmain.clear();
   P.pos_br.clear();
   P.rope_freq.clear();
+  P.rope_rad.clear();
   if (theta > 0.f) {
     const int32_t C = P.cp_size;
     int64_t max_pos = 0;
@@ -429,6 +435,8 @@ static int build_rope(Plan& P, float theta) {
     }
     P.rope_freq.resize(kHeadDim / 2);
     rope_freq_table(theta, P.rope_freq.data());
+    P.rope_rad.resize(kHeadDim / 2);
+    rope_rad_table(theta, P.rope_rad.data());
   }
   pack_image(P);
   return BA_OK;

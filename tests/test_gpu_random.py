@@ -9,6 +9,11 @@ A second generator draws sequences of up to 2048 tokens (walks of up to 32
 key tiles per ring block), DFlash blocks up to 64 and the plan's own
 schedule choice as a third mode; its seeds are a spread over CP sizes 1-8,
 schedules, layouts and rotary settings whose oracle finishes in seconds.
+Seed 557 (two sequences of 1722 and 888 tokens, C = 3, 32/8 heads, rotary
+base 1e4) is the draw on which rotated inputs rounded to bf16 from a float
+rotation differed from the double-precision definition in about 3 in 10^5
+values and moved a branch row's LSE by 1.3e-3; the input rotation now
+rounds from double.
 """
 
 import numpy as np
@@ -128,7 +133,7 @@ def test_random_problem_parity(cuda, seed):
     run_case(f"random {seed}", prob, o)
 
 
-@pytest.mark.parametrize("seed", [1, 2, 3, 5, 7, 8, 13, 14, 24, 30, 33, 35, 40, 46, 52, 56])
+@pytest.mark.parametrize("seed", [1, 2, 3, 5, 7, 8, 13, 14, 24, 30, 33, 35, 40, 46, 52, 56, 557])
 def test_random_long_problem_parity(cuda, seed):
     prob, o = draw_long_case(seed)
     run_case(f"random long {seed}", prob, o)
