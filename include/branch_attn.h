@@ -215,7 +215,8 @@ void branch_attn_plan_destroy(ba_plan* plan);
  * i + 1 of a DFlash block, after its anchor).  Dims j and j + 64 (j < 64)
  * turn together by the angle pos * theta^(-j/64) (x_j' = x_j cos - x_{j+64}
  * sin, x_{j+64}' = x_{j+64} cos + x_j sin); the rotated queries and keys are
- * rounded to bf16 (RNE) before attending, values are not rotated.
+ * evaluated in double (angle, sine, cosine, products) and rounded once to
+ * bf16 (RNE) before attending, values are not rotated.
  * With theta > 0 every later branch_attn_fwd / branch_attn_bwd call on the
  * plan attends the rotated queries and keys, and the backward returns dQ and
  * dK with respect to the unrotated inputs (the transposed rotation of the
