@@ -818,7 +818,17 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(BwdParams p) {
       for (int b = 0; b < BA_MAX_GROUP_LEN; ++b) {
         if (__ballot(b < nb) == 0) break;
         const int bu = min(b, max(nb - 1, 0));
-        const int64_t krow = (int64_t)gi.row0 + (int64_t)bu * gi.stride;
+        int64_t krow = (int64_t)gi.row0 + (int64_t)bu * gi.stride;
+        // a row without branch keys (a main row) reads the key of the
+        // wavefront's first lane that has one: its weight is zero, and the
+        // row it would read otherwise (branch row 0) may belong to no group
+        // and hold anything (zero times a non-finite value is not zero)
+        {
+          const int src = __builtin_ctzll(__ballot(b < nb));  // the loop runs while some lane has a key
+          const int lo = __builtin_amdgcn_readlane((int)(krow & 0xffffffff), src);
+          const int hi = __builtin_amdgcn_readlane((int)(krow >> 32), src);
+          if (nb == 0) krow = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+        }
         const bf16* kb = p.k_br + krow * kv_row_stride + tile.kvh * kHeadDim;
         const bf16* vb = p.v_br + krow * kv_row_stride + tile.kvh * kHeadDim;
         bf16x8 kd[8], vd[8];
@@ -1242,7 +1252,11 @@ __global__ __launch_bounds__(256) void bwd_dq_finalize_kernel(BwdParams p) {
         }
         sd = row16_sum(sd);
         pd = row16_sum(pd);
-        const float pr = b0 + u < nb ? fast_exp2(fmaf(sd, p.scale_log2, rs.x)) : 0.f;
+        // (after the row sums, which every lane takes part in) a row without
+        // this key adds nothing: a main row read branch row 0, which may
+        // belong to no group and hold anything
+        if (b0 + u >= nb) continue;
+        const float pr = fast_exp2(fmaf(sd, p.scale_log2, rs.x));
         const float ds = pr * (pd + rs.y);
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = fmaf(ds, (float)kv[u][e], acc[e]);

@@ -137,3 +137,17 @@ def test_random_problem_parity(cuda, seed):
 def test_random_long_problem_parity(cuda, seed):
     prob, o = draw_long_case(seed)
     run_case(f"random long {seed}", prob, o)
+
+
+@pytest.mark.parametrize("mode", ["fused", "per_step"])
+def test_unused_branch_rows_are_never_summed(cuda, mode):
+    """Short draw 200 (depth layout, rotary embedding on): branch row 0 belongs
+    to no group, so its rotated copy is never written, and main rows of a
+    query tile whose branch keys are read from global memory once read it
+    with weight zero.  Freed device memory is filled with NaN first, so such a
+    row reaching a sum shows as a non-finite gradient."""
+    prob, o = draw_case(200)
+    junk = [torch.full((n,), float("nan"), device="cuda") for n in (1 << 24, 1 << 26, 1 << 28)]
+    del junk
+    torch.cuda.synchronize()
+    run_case(f"unused rows {mode}", prob, dict(o, mode=mode))
