@@ -38,12 +38,12 @@ PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 4096 dense bf16 FLOP/c
 # taken on the same sources), scaled by a plain-copy calibration.  A figure
 # only applies while the kernel's source is the one that was measured.
 MEASURED_TRAFFIC = {
-    ("bwd_kv_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "aaa071043f927a61", "bytes": 9966748580},
-    ("bwd_dq_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "aaa071043f927a61", "bytes": 39637991783},
-    ("fwd_kernel", "fused"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 37983852968},
-    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "aaa071043f927a61", "bytes": 9962493511},
-    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "aaa071043f927a61", "bytes": 7815872132},
-    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 7168797737},
+    ("bwd_kv_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "f3011df620efb2e7", "bytes": 9961742616},
+    ("bwd_dq_kernel", "fused"): {"source": "bwd.hip", "sha256_16": "f3011df620efb2e7", "bytes": 38219996059},
+    ("fwd_kernel", "fused"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 37982780076},
+    ("bwd_kv_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "f3011df620efb2e7", "bytes": 9976401605},
+    ("bwd_dq_kernel", "per_step"): {"source": "bwd.hip", "sha256_16": "f3011df620efb2e7", "bytes": 7824389477},
+    ("fwd_kernel", "per_step"): {"source": "fwd.hip", "sha256_16": "0b9b2bab93598c2e", "bytes": 7168648699},
 }
 
 def measured_traffic(kernel: str, workload: str, mode: str):
